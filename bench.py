@@ -1,0 +1,224 @@
+"""Benchmark: WAMachine-style replans on one MI355X.
+
+A timed step is one closed-loop replan of the small joint video/action DiT
+(12 layers, hidden 768, 12 heads, MLP 3072; 768 video + 32 action + 64
+observation tokens; 10 flow steps; bf16 contractions): Trajectory Remapping of
+the previous replan's state, an anticipatory prefix of 2 steps under the
+predicted observation, the consistency score and rebinding (or restart), and
+Residual Rescaling inside every denoising step, all through libwam.  Inputs
+(weights, noise, AR(1) observations) are seeded, synthetic and resident in HBM
+before timing starts.
+
+Prints one JSON line.  --gpus N > 1 is refused: this build runs on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=30)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="replay", help="replay (small model) | mid | large")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-native", action="store_true")
+    p.add_argument("--cpu-sample-steps", type=int, default=5)
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); multi-GPU runs are not part "
+              "of this build.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2609_34608_amd import _lib as L
+    from paper_2609_34608_amd import runtime as R
+    from synth import get_workload, make_weights, make_initial_noise, make_observations, make_remap_noise
+
+    spec = get_workload(args.workload)
+    dev = torch.device("cuda:0")
+    W = make_weights(spec)
+    m = R.WamModel(R.config_of(spec), W, device=dev)
+    K = spec.K
+    s = np.arange(K + 1, dtype=np.float64)
+    sig = (1.0 - s / K)  # uniform flow schedule sigma_k = 1 - k/K
+    m.set_schedule(sig)
+    q, s_, e = spec.rr_bounds
+    rr = R.rr_profile(q, s_, e, L.WAM_RR_AUTO, spec.rr_alpha_min, spec.rr_alpha_max, spec.rr_eps,
+                      spec.rr_gamma_cos, spec.rr_gamma_fit)
+    n_ctrl = 1 + args.warmup + args.steps
+    obs = make_observations(spec, n_ctrl)
+    rho = spec.ar_rho
+    delta = 1.0 / np.sqrt(1.0 - rho * rho)
+    obs_d = torch.from_numpy(obs).to(dev)
+    pred_d = torch.from_numpy((rho * obs[:-1]).astype(np.float32)).to(dev)
+    noise_first = torch.from_numpy(make_initial_noise(spec)).to(dev)
+    remap_noise = torch.from_numpy(np.stack([make_remap_noise(spec, t) for t in range(n_ctrl)])).to(dev)
+    x_out = m.new_traj()
+    ra = dict(b0=spec.tr_b0, r=spec.tr_r, shift_action=spec.shift_action, shift_video=spec.shift_video,
+              k1=spec.or_k1, tau=spec.or_tau, kappa_max=spec.or_kappa_max)
+
+    def replan(t):
+        cr = obs_d[t]
+        cp = pred_d[t - 1] if t > 0 else obs_d[t]
+        return m.replan(cr, x_out, remap_noise[t], cond_pred=cp, u_hat=[cp], u=[cr], delta=[delta],
+                        weight=[1.0], noise_first=noise_first, rr=rr, **ra)
+
+    torch.cuda.synchronize()
+    t = 0
+    replan(t)  # first replan: native K steps from noise
+    t += 1
+    for _ in range(args.warmup):
+        replan(t)
+        t += 1
+    # untimed attribution pass over one replan: which kernel class dominates
+    classes = [L.WAM_KC_GEMM_QKV, L.WAM_KC_GEMM_PROJ, L.WAM_KC_GEMM_FC1, L.WAM_KC_GEMM_FC2,
+               L.WAM_KC_ATTENTION]
+    for kc in classes:
+        m.profile_enable(kc, True, 4096)
+    replan(t - 1 if t > 1 else t)
+    tot = {kc: m.profile_read(kc)[0] for kc in classes}
+    for kc in classes:
+        m.profile_enable(kc, False)
+    dom = max(tot, key=tot.get)
+    m.reset_all()
+    replan(0)
+    for tt in range(1, t):
+        replan(tt)
+    # timed region: events around the dominant kernel's launches only
+    m.profile_enable(dom, True, 200000)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    infos = []
+    for _ in range(args.steps):
+        infos.append(replan(t))
+        t += 1
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    dom_ms, dom_n, dom_work = m.profile_read(dom)
+    m.profile_enable(dom, False)
+
+    n_steps = sum(i.steps for i in infos)
+    layers_eval = sum(i.steps * spec.L - i.layers_skipped for i in infos)
+    flops = spec.flops_per_layer() * layers_eval
+    ms_per_step = 1000.0 * elapsed / args.steps
+    steps_per_s = n_steps / elapsed
+    chunks_per_s = args.steps / elapsed
+    n_att = sum(i.rr_attempts for i in infos)
+    n_reuse = sum(i.rr_reuses for i in infos)
+    skip = sum(i.layers_skipped for i in infos)
+    dense = sum(i.layers_dense for i in infos)
+    n_start = sum(i.n_start for i in infos)
+    n_bind = sum(i.n_bind for i in infos)
+
+    dom_tflops = dom_work / (dom_ms * 1e-3) / 1e12 if dom_ms > 0 else 0.0
+    out = {
+        "metric": "denoise steps/s + action chunks/s per MI355X; MFMA % of bf16 peak",
+        "value": round(steps_per_s, 3),
+        "unit": "denoise steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if spec.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded random-init weights N(0,0.02), N(0,1) noise, AR(1) observations)",
+        "config": {
+            "workload": (f"{spec.name}: closed-loop replan with TR+OR+RR on a joint video/action DiT "
+                         f"B{spec.B} L{spec.L} D{spec.D} H{spec.H} F{spec.F} T{spec.T} "
+                         f"(video {spec.Nv}, action {spec.Na}x{spec.A}, obs {spec.No}) K{spec.K} "
+                         f"b0={spec.tr_b0} k1={spec.or_k1} shift={spec.shift_action}"),
+            "step": "one replan (control step)",
+        },
+        "action_chunks_per_s": round(chunks_per_s, 3),
+        "denoise_steps_per_replan": n_steps / args.steps,
+        "mfma_frac_dit": round(flops / elapsed / 1e12 / MFMA_BF16_PEAK_TFLOPS, 5),
+        "dit_tflops": round(flops / elapsed / 1e12, 3),
+        "reuse_stats": {"rr_accept": n_reuse / n_att if n_att else None,
+                        "rr_skip_frac": skip / dense if dense else None,
+                        "or_accept": n_bind / n_start if n_start else None,
+                        "or_coverage": n_bind / args.steps},
+        "roofline": {
+            "kernel": L.KERNEL_CLASS_NAMES[dom],
+            "bound": "mfma",
+            "achieved": round(dom_tflops, 3),
+            "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(dom_tflops / MFMA_BF16_PEAK_TFLOPS, 5),
+            "traffic": None,
+            "launches": dom_n,
+            "avg_launch_us": round(1000.0 * dom_ms / dom_n, 3) if dom_n else None,
+            "class_ms_one_replan": {L.KERNEL_CLASS_NAMES[k]: round(v, 4) for k, v in tot.items()},
+        },
+    }
+
+    if not args.no_native:
+        # full re-denoise of the same model: K native steps from noise per chunk
+        xn = m.new_traj()
+        nrep = max(3, args.steps // 5)
+        m.reset_all()
+        xn.copy_(noise_first)
+        m.continue_(0, K, xn, obs_d[0])
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(nrep):
+            xn.copy_(noise_first)
+            m.continue_(0, K, xn, obs_d[i + 1])
+        torch.cuda.synchronize()
+        nat = (time.perf_counter() - t0) / nrep
+        out["native_chunk_ms"] = round(1000.0 * nat, 4)
+        out["native_steps_per_s"] = round(K / nat, 3)
+        out["reuse_latency_speedup"] = round(nat / (elapsed / args.steps), 4)
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(spec, W, obs, args.cpu_sample_steps)
+    print(json.dumps(out), flush=True)
+    m.close()
+
+
+def cpu_baseline(spec, W, obs, n_steps):
+    """The float64 oracle on the host: a bounded sample of Euler steps of the
+    same model (the continuation of one accepted replan), timed."""
+    import numpy as np
+    from oracle import method as OM
+    from synth import make_initial_noise
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:
+        threads = os.cpu_count() or 1
+    sig = OM.flow_schedule(spec.K)
+    q, s, e = spec.rr_bounds
+    rr = OM.RRProfile(q, s, e, spec.rr_alpha_min, spec.rr_alpha_max, spec.rr_eps, spec.rr_gamma_cos,
+                      spec.rr_gamma_fit)
+    x = make_initial_noise(spec)
+    k0 = spec.K - n_steps
+    t0 = time.perf_counter()
+    OM.denoise(W, spec, x, obs[0], sig, k0, spec.K, rr, OM.LayerState())
+    dt = time.perf_counter() - t0
+    return {"value": round(n_steps / dt, 5), "unit": "denoise steps/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{n_steps} float64 Euler steps with residual rescaling of the same model "
+                      f"(steps {k0}..{spec.K - 1}), {dt:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,280 @@
+/*
+ * libwam — MI355X (gfx950) hot path of training-free World Action Model
+ * inference with adaptive intermediate states.
+ *
+ * The library runs the iterative flow-denoising step of a DiT-style joint
+ * video-latent + action-token transformer, and the three state-adaptation
+ * operators that let a replan continue from retained state instead of
+ * re-denoising from noise:
+ *
+ *   Trajectory Remapping  (Sec. 3.1, Eq. direction and Eq. transport, with the
+ *                          unit-RMS normalisation of Eq. app-transport-rms),
+ *   Observation Rebinding (Sec. 3.2, Eq. bind-discrepancy and the kappa rule),
+ *   Residual Rescaling    (Sec. 3.3, Eq. crr-reference, crr-alpha, crr-gate,
+ *                          residual-injection and refresh on failure),
+ *
+ * coordinated as in Sec. 3.4 (joint runtime).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Ownership: the caller allocates every device buffer (packed weights,
+ *    workspace, trajectories, conditions, noise, outputs) and keeps it alive
+ *    while the handle uses it.  The library never allocates device memory; the
+ *    retained-state cache lives inside the caller's workspace.  Host pointers
+ *    are only read during the call.
+ *  - Streams: all device work is enqueued on the hipStream_t given to
+ *    wam_init.  Calls that need a host-side decision (Residual Rescaling gate,
+ *    Observation Rebinding score) synchronise that stream before returning;
+ *    the others are asynchronous.
+ *  - Randomness: the library draws no random numbers.  Noise is an input.
+ *  - Layouts (all row-major, all device float32 unless stated):
+ *      trajectory  x [B][traj], traj = Nv*Cv + Na*A, per sample
+ *                  [video tokens (Nv x Cv) | action tokens (Na x A)];
+ *      condition   cond [B][No][Co] (observation-conditioning tokens);
+ *      hidden      h [B][T][D] with T = Nv + Na + No rows ordered
+ *                  [video | action | observation].
+ *  - Errors: every int-returning call returns WAM_OK (0) or a negative status
+ *    and, given a handle, stores a message for wam_last_error.  Nothing throws
+ *    across the ABI.  A failing call leaves retained state unchanged unless
+ *    documented otherwise.
+ *  - Threading: a handle is used by one host thread at a time.
+ */
+#ifndef WAM_H
+#define WAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------- */
+#define WAM_OK 0
+#define WAM_E_ARG (-1)         /* invalid scalar argument or null pointer     */
+#define WAM_E_SHAPE (-2)       /* model dimensions not supported / mismatched */
+#define WAM_E_STATE (-3)       /* call not valid in the handle's state        */
+#define WAM_E_HIP (-4)         /* HIP runtime error                           */
+#define WAM_E_WORKSPACE (-5)   /* weight or workspace buffer too small        */
+#define WAM_E_UNSUPPORTED (-6) /* valid request this build does not implement */
+
+/* ---- numeric modes --------------------------------------------------- */
+#define WAM_FP32 0 /* all activations and contractions in float32            */
+#define WAM_BF16 1 /* projection / attention operands bf16, fp32 accumulate;
+                      residual stream, trajectory, layer state, norms and all
+                      reductions stay float32 (or float64 for gate sums)      */
+
+/* ---- Residual Rescaling modes ------------------------------------------ */
+#define WAM_RR_OFF 0        /* plain full forward, no layer state kept        */
+#define WAM_RR_AUTO 1       /* gate of Eq. crr-gate decides reuse or refresh  */
+#define WAM_RR_FORCE_SKIP 2 /* reuse whenever a layer state exists            */
+#define WAM_RR_FORCE_FULL 3 /* always compute the middle and refresh          */
+
+/* ---- wam_adapt_state operations ---------------------------------------- */
+#define WAM_ADAPT_REMAP 1       /* args: const wam_remap_args*               */
+#define WAM_ADAPT_RESET_LAYER 2 /* args: NULL; drop retained (p_a, R_a)      */
+#define WAM_ADAPT_RESET_ALL 3   /* args: NULL; drop layer and replan state   */
+#define WAM_ADAPT_SET_REPLAN 4  /* args: const wam_replan_state_args*        */
+
+/* ---- replan paths (Sec. 3.4) ------------------------------------------- */
+#define WAM_PATH_FIRST 0  /* first replan: K steps from fresh noise           */
+#define WAM_PATH_ACCEPT 1 /* prefix under the predicted condition, rebound    */
+#define WAM_PATH_REJECT 2 /* prefix failed the check: restart under c         */
+#define WAM_PATH_FORCED 3 /* kappa reached kappa_max: refresh, no prefix      */
+#define WAM_PATH_DIRECT 4 /* rebinding disabled: K-b0 steps under c           */
+
+#define WAM_MAX_BATCH 16
+#define WAM_MAX_COMPONENTS 8
+#define WAM_MAX_STEPS 64
+
+/* Kernel classes for wam_profile_* (per-launch HIP-event timing). */
+#define WAM_KC_GEMM_QKV 0
+#define WAM_KC_GEMM_PROJ 1
+#define WAM_KC_GEMM_FC1 2
+#define WAM_KC_GEMM_FC2 3
+#define WAM_KC_ATTENTION 4
+#define WAM_KC_RR_GATE 5
+#define WAM_KC_RR_INJECT 6
+#define WAM_KC_RR_REFRESH 7
+#define WAM_KC_COUNT 8
+
+typedef struct wam_handle *wam_t;
+
+/* Model configuration.  D % H == 0, head size D/H in {32, 64};
+ * bf16 mode additionally needs D/H == 64, D % 128 == 0, F % 128 == 0. */
+typedef struct {
+  int32_t B;       /* batch (samples denoised together), 1..WAM_MAX_BATCH */
+  int32_t L;       /* DiT layers                                            */
+  int32_t D;       /* hidden size                                           */
+  int32_t H;       /* attention heads                                       */
+  int32_t F;       /* MLP hidden size                                       */
+  int32_t Nv, Cv;  /* video-latent tokens, channels per token               */
+  int32_t Na, A;   /* action tokens (chunk length), action dimension        */
+  int32_t No, Co;  /* observation tokens, channels per token                */
+  int32_t dtype;   /* WAM_FP32 | WAM_BF16                                   */
+  int32_t qk_norm; /* 1: RMS-normalise q and k per head (with gains)        */
+  float ln_eps;    /* epsilon of LayerNorm and QK RMSNorm                   */
+} wam_config;
+
+/* Residual Rescaling profile (Sec. 3.3; thresholds as in Table app-guards).
+ * Layer boundaries 0 < q < s < e < L partition the DiT into head [0,q),
+ * probe [q,s), middle [s,e) and tail [e,L). */
+typedef struct {
+  int32_t q, s, e;
+  int32_t mode; /* WAM_RR_* */
+  float alpha_min, alpha_max, eps;
+  float gamma_cos, gamma_fit;
+} wam_rr_profile;
+
+/* Per-denoising-step report.  alpha/cos/fit are per sample and per branch
+ * (branch 0 = video and observation rows, 1 = action rows); valid when
+ * rr_attempted. */
+typedef struct {
+  int32_t rr_active;    /* RR mode was not OFF                              */
+  int32_t rr_attempted; /* a retained state existed and the gate was run    */
+  int32_t rr_accepted;  /* the middle layers were skipped                   */
+  int32_t layers_evaluated;
+  int32_t layers_skipped;
+  int32_t reserved;
+  double alpha[WAM_MAX_BATCH][2];
+  double cos[WAM_MAX_BATCH][2];
+  double fit[WAM_MAX_BATCH][2];
+} wam_step_info;
+
+/* Trajectory Remapping arguments (Eq. direction, Eq. transport). */
+typedef struct {
+  const float *x_bar; /* device [B][traj]: final output of the previous replan  */
+  const float *x_r;   /* device [B][traj]: latent retained at stage r           */
+  float sigma_r;      /* noise level of stage r, must be > 0                    */
+  float sigma_b0;     /* noise level of the entry stage b0                      */
+  int32_t shift_action; /* target action slot j takes source slot j+shift (>=0) */
+  int32_t shift_video;  /* same for video tokens (>=0)                          */
+  const float *noise; /* device [B][traj] N(0,1); unmapped slots get sigma_b0*noise */
+  float *x_out;       /* device [B][traj]: remapped initialisation              */
+} wam_remap_args;
+
+/* Adopt an externally held replan state (teacher forcing / resume). */
+typedef struct {
+  const float *x_bar; /* device [B][traj] */
+  const float *x_r;   /* device [B][traj] */
+  int32_t kappa;
+} wam_replan_state_args;
+
+/* One closed-loop replan (Sec. 3.4). */
+typedef struct {
+  const float *cond_real; /* device [B][No][Co]: real condition c_{t+1}          */
+  const float *cond_pred; /* device [B][No][Co]: predicted condition (OR prefix) */
+  /* consistency components compared before encoding (Eq. bind-discrepancy) */
+  int32_t n_components;
+  const float *u_hat[WAM_MAX_COMPONENTS]; /* device, n[m] floats each         */
+  const float *u[WAM_MAX_COMPONENTS];
+  int64_t n[WAM_MAX_COMPONENTS];
+  double delta[WAM_MAX_COMPONENTS];
+  double weight[WAM_MAX_COMPONENTS];
+  const float *noise_first; /* device [B][traj] N(0,1): first replan's x at sigma_0 */
+  const float *noise_remap; /* device [B][traj] N(0,1): unmapped slots / fresh init */
+  float *x_out;             /* device [B][traj]: receives the new x_bar             */
+  wam_rr_profile rr;
+  int32_t b0, r;             /* entry stage and retained stage, b0 <= r < K    */
+  int32_t shift_action, shift_video;
+  int32_t k1;                /* anticipatory prefix steps, 0 < k1 < K-b0       */
+  double tau;                /* accept iff S < tau and kappa < kappa_max       */
+  int32_t kappa_max;
+  int32_t tr_enabled, or_enabled;
+  int32_t rr_first, rr_prefix, rr_refresh; /* RR allowed on each path       */
+} wam_replan_args;
+
+typedef struct {
+  int32_t path;  /* WAM_PATH_* */
+  int32_t kappa; /* after this replan */
+  int32_t steps; /* denoising steps executed (prefix + continuation/restart) */
+  int32_t n_start, n_bind; /* 0/1 for this replan (Eq. app-rebinding-rates) */
+  int32_t rr_attempts, rr_reuses, layers_skipped, layers_dense;
+  int32_t reserved;
+  double S; /* consistency score, or -1 when no prefix was checked */
+  int8_t decision[WAM_MAX_STEPS]; /* per step: -1 no attempt, 0 refresh, 1 reuse */
+} wam_replan_info;
+
+/* ---- sizes --------------------------------------------------------------- */
+/* Number of float32 values of the canonical host weight buffer, which holds,
+ * each row-major with Linear weights stored [in][out] (y = x W + b):
+ *   t_w1[256][D] t_b1[D] t_w2[D][D] t_b2[D]
+ *   in_wv[Cv][D] in_bv[D] in_wa[A][D] in_ba[D] in_wo[Co][D] in_bo[D]
+ *   for each layer l: mod_w[D][6D] mod_b[6D] qkv_w[D][3D] qkv_b[3D]
+ *                     q_g[dh] k_g[dh] proj_w[D][D] proj_b[D]
+ *                     fc1_w[D][F] fc1_b[F] fc2_w[F][D] fc2_b[D]
+ *   f_mod_w[D][2D] f_mod_b[2D] out_wv[D][Cv] out_bv[Cv] out_wa[D][A] out_ba[A]
+ * Returns 0 for an invalid configuration. */
+size_t wam_host_weight_count(const wam_config *cfg);
+/* Device bytes of the packed weights and of the workspace (0 if invalid). */
+size_t wam_weight_bytes(const wam_config *cfg);
+size_t wam_workspace_bytes(const wam_config *cfg);
+/* Trajectory elements per sample, Nv*Cv + Na*A. */
+int64_t wam_traj_elems(const wam_config *cfg);
+
+/* ---- lifetime ------------------------------------------------------------ */
+/* Validates cfg, converts and packs the host weights (bf16 mode: projection
+ * and modulation matrices rounded to bf16, nearest-even) into dev_weights,
+ * carves the workspace, and returns a handle.  Synchronous. */
+int wam_init(const wam_config *cfg, const float *host_weights, size_t n_host_weights,
+             void *dev_weights, size_t weight_bytes, void *dev_workspace,
+             size_t workspace_bytes, void *hip_stream, wam_t *out);
+void wam_destroy(wam_t h);
+int wam_sync(wam_t h);
+const char *wam_last_error(wam_t h);
+const char *wam_status_string(int status);
+
+/* Noise levels sigma_0 = 1 > ... > sigma_K = 0 of the flow schedule
+ * (host float[K+1]); K <= WAM_MAX_STEPS.  Required before any step. */
+int wam_set_schedule(wam_t h, const float *sigmas, int K);
+
+/* ---- denoising ------------------------------------------------------------ */
+/* Denoiser prediction v(x, sigma_k, cond) into v_out [B][traj]; runs the
+ * embedding, the L DiT layers (with Residual Rescaling per rr, which may be
+ * NULL = off), the final layer and the output heads.  Updates the retained
+ * layer state as Sec. 3.3 prescribes. */
+int wam_velocity(wam_t h, int k, const float *x, const float *cond, float *v_out,
+                 const wam_rr_profile *rr, wam_step_info *info);
+/* One Euler step of the flow ODE: x <- x + (sigma_{k+1} - sigma_k) v. */
+int wam_denoise_step(wam_t h, int k, float *x, const float *cond,
+                     const wam_rr_profile *rr, wam_step_info *info);
+/* Steps k_from .. k_to-1 in place on x.  If k_from <= capture_stage <= k_to
+ * the latent at that stage is copied to x_capture (device [B][traj]).
+ * infos may be NULL or hold k_to - k_from entries. */
+int wam_continue(wam_t h, int k_from, int k_to, float *x, const float *cond,
+                 const wam_rr_profile *rr, int capture_stage, float *x_capture,
+                 wam_step_info *infos);
+/* Hidden state after the first n_layers layers (no RR) at stage k into
+ * h_out [B][T][D]; for layer-level parity checks. */
+int wam_hidden(wam_t h, int k, const float *x, const float *cond, int n_layers, float *h_out);
+
+/* ---- state adaptation ------------------------------------------------------ */
+int wam_adapt_state(wam_t h, int op, const void *args);
+/* Observation Rebinding score (Eq. bind-discrepancy) over device arrays,
+ * accumulated in float64: S = sqrt(sum w e^2 / sum w),
+ * e_m = sqrt(mean(((u_hat_m - u_m)/delta_m)^2)).  Synchronises. */
+int wam_consistency_score(wam_t h, int n_components, const float *const *u_hat,
+                          const float *const *u, const int64_t *n, const double *delta,
+                          const double *weight, double *S_out);
+/* One replan of the joint runtime.  The first call (or after RESET_ALL) runs
+ * the native K steps from noise_first; later calls apply Trajectory
+ * Remapping, the anticipatory prefix under cond_pred, the consistency check
+ * and rebinding or restart, with Residual Rescaling inside each step.  The
+ * retained replan state (x_bar, x^r, kappa) lives in the workspace. */
+int wam_replan(wam_t h, const wam_replan_args *args, wam_replan_info *info);
+/* Copies of the retained replan state (device [B][traj] each; may be NULL). */
+int wam_get_replan_state(wam_t h, float *x_bar, float *x_r, int32_t *kappa);
+
+/* ---- measurement ------------------------------------------------------------ */
+/* Record a HIP event pair around every launch of kernel class kc (WAM_KC_*),
+ * up to max_launches launches, on the handle's stream.  enable = 0 stops. */
+int wam_profile_enable(wam_t h, int kc, int enable, int max_launches);
+/* Sum of launch durations (ms), launch count and algorithmic work (FLOP for
+ * contractions, bytes for streaming kernels) of the recorded launches.
+ * Synchronises. */
+int wam_profile_read(wam_t h, int kc, double *total_ms, int64_t *launches, double *work);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WAM_H */

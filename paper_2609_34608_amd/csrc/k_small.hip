@@ -1,0 +1,494 @@
+// Bandwidth- and latency-bound kernels of the denoising step and of the
+// state-adaptation operators (gfx950, wave64).
+#include <math.h>
+
+#include "wam_internal.h"
+
+namespace wam {
+
+namespace {
+
+constexpr int kMaxVpl = 32;  // row kernels hold D/64 <= 32 values per lane
+
+__device__ __forceinline__ double block_sum_d(double v, double* sh) {
+  v = wave_sum_d(v);
+  const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int nw = blockDim.x / kWave;
+  __syncthreads();
+  if (lane == 0) sh[w] = v;
+  __syncthreads();
+  double t = 0.0;
+  for (int i = 0; i < nw; ++i) t += sh[i];
+  return t;
+}
+
+// ------------------------------------------------------------- timestep
+// e = [cos(t f_i), sin(t f_i)], t = 1000 sigma, f_i = 10000^(-i/half)
+__global__ void timestep_features_kernel(float sigma, float* e, int dim) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  const int half = dim / 2;
+  if (i >= dim) return;
+  const int j = i < half ? i : i - half;
+  const double t = 1000.0 * (double)sigma;
+  const double f = exp(-log(10000.0) * (double)j / (double)half);
+  e[i] = (float)(i < half ? cos(t * f) : sin(t * f));
+}
+
+// ------------------------------------------------------------- GEMV
+constexpr int kGemvKc = 32;   // input rows per split
+constexpr int kGemvVec = 4;   // outputs per thread
+
+__device__ __forceinline__ float act_apply(float v, int act) {
+  return act == 1 ? v / (1.0f + __expf(-v)) : v;
+}
+
+template <typename TW>
+__global__ void gemv_partial_kernel(const float* __restrict__ x, const TW* __restrict__ W,
+                                    float* __restrict__ partial, int K, int N, int in_act) {
+  const int n0 = (blockIdx.x * blockDim.x + threadIdx.x) * kGemvVec;
+  const int k0 = blockIdx.y * kGemvKc;
+  if (n0 >= N) return;
+  float acc[kGemvVec] = {0.f, 0.f, 0.f, 0.f};
+  const int k1 = min(K, k0 + kGemvKc);
+  for (int k = k0; k < k1; ++k) {
+    const float xv = act_apply(x[k], in_act);
+    const TW* row = W + (size_t)k * N + n0;
+#pragma unroll
+    for (int j = 0; j < kGemvVec; ++j) acc[j] += xv * to_f32(row[j]);
+  }
+  float* p = partial + (size_t)blockIdx.y * N + n0;
+#pragma unroll
+  for (int j = 0; j < kGemvVec; ++j) p[j] = acc[j];
+}
+
+__global__ void gemv_reduce_kernel(const float* __restrict__ partial, const float* __restrict__ b,
+                                   float* __restrict__ y, int nchunk, int N, int out_act) {
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= N) return;
+  float s = 0.f;
+  for (int c = 0; c < nchunk; ++c) s += partial[(size_t)c * N + n];
+  y[n] = act_apply(s + b[n], out_act);
+}
+
+// ------------------------------------------------------------- embedding
+// h[b,t,:] = token (video | action | obs) @ W_branch + b_branch + PE(t)
+__global__ void embed_kernel(EmbedArgs a) {
+  const int row = blockIdx.x;  // b*T + t
+  const int b = row / a.T, t = row % a.T;
+  __shared__ float tok[64];
+  const float* w;
+  const float* bias;
+  int c;
+  const int traj = a.Nv * a.Cv + a.Na * a.A;
+  if (t < a.Nv) {
+    c = a.Cv;
+    w = a.wv;
+    bias = a.bv;
+    if (threadIdx.x < c) tok[threadIdx.x] = a.x[(size_t)b * traj + (size_t)t * a.Cv + threadIdx.x];
+  } else if (t < a.Nv + a.Na) {
+    c = a.A;
+    w = a.wa;
+    bias = a.ba;
+    if (threadIdx.x < c)
+      tok[threadIdx.x] = a.x[(size_t)b * traj + (size_t)a.Nv * a.Cv + (size_t)(t - a.Nv) * a.A + threadIdx.x];
+  } else {
+    c = a.Co;
+    w = a.wo;
+    bias = a.bo;
+    if (threadIdx.x < c)
+      tok[threadIdx.x] = a.cond[((size_t)b * a.No + (t - a.Nv - a.Na)) * a.Co + threadIdx.x];
+  }
+  __syncthreads();
+  const int half = a.D / 2;
+  for (int d = threadIdx.x; d < a.D; d += blockDim.x) {
+    float s = bias[d];
+    for (int j = 0; j < c; ++j) s += tok[j] * w[(size_t)j * a.D + d];
+    const int jj = d < half ? d : d - half;
+    const double om = exp(-log(10000.0) * (double)jj / (double)half);
+    const double ang = (double)t * om;
+    s += (float)(d < half ? sin(ang) : cos(ang));
+    a.h[(size_t)row * a.D + d] = s;
+  }
+}
+
+// ------------------------------------------------------------- LN + modulation
+// One wave per row; lane holds elements lane + 64 i.
+template <typename TOut>
+__global__ void ln_modulate_kernel(const float* __restrict__ h, const float* __restrict__ shift,
+                                   const float* __restrict__ scale, TOut* __restrict__ u,
+                                   int rows, int D, float eps) {
+  const int row = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  if (row >= rows) return;
+  const float* hr = h + (size_t)row * D;
+  const int vpl = D / kWave;
+  float v[kMaxVpl];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxVpl; ++i) {
+    if (i < vpl) {
+      v[i] = hr[lane + kWave * i];
+      s += v[i];
+    }
+  }
+  const float mean = wave_sum(s) / (float)D;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxVpl; ++i)
+    if (i < vpl) {
+      const float d = v[i] - mean;
+      q += d * d;
+    }
+  const float rstd = rsqrtf(wave_sum(q) / (float)D + eps);
+  TOut* ur = u + (size_t)row * D;
+#pragma unroll
+  for (int i = 0; i < kMaxVpl; ++i)
+    if (i < vpl) {
+      const int c = lane + kWave * i;
+      ur[c] = from_f32<TOut>((v[i] - mean) * rstd * (1.0f + scale[c]) + shift[c]);
+    }
+}
+
+// ------------------------------------------------------------- final layer + Euler
+// One wave per trajectory row (video or action token): LN + final
+// modulation, output head (W^T packed [Cout][D]), optional velocity store and
+// fused Euler update x += dsigma * v.
+__global__ void final_kernel(FinalArgs a, const float* __restrict__ wvT,
+                             const float* __restrict__ waT) {
+  const int nrow = a.Nv + a.Na;
+  const int gw = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  if (gw >= a.B * nrow) return;
+  const int b = gw / nrow, t = gw % nrow;
+  const float* hr = a.h + ((size_t)b * a.T + t) * a.D;
+  const int vpl = a.D / kWave;
+  float v[kMaxVpl];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxVpl; ++i)
+    if (i < vpl) {
+      v[i] = hr[lane + kWave * i];
+      s += v[i];
+    }
+  const float mean = wave_sum(s) / (float)a.D;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxVpl; ++i)
+    if (i < vpl) {
+      const float d = v[i] - mean;
+      q += d * d;
+    }
+  const float rstd = rsqrtf(wave_sum(q) / (float)a.D + a.eps);
+#pragma unroll
+  for (int i = 0; i < kMaxVpl; ++i)
+    if (i < vpl) {
+      const int c = lane + kWave * i;
+      v[i] = (v[i] - mean) * rstd * (1.0f + a.scale[c]) + a.shift[c];
+    }
+  const bool video = t < a.Nv;
+  const int cout = video ? a.Cv : a.A;
+  const float* wT = video ? wvT : waT;
+  const float* bias = video ? a.bv : a.ba;
+  const int traj = a.Nv * a.Cv + a.Na * a.A;
+  const size_t base = (size_t)b * traj + (video ? (size_t)t * a.Cv
+                                                : (size_t)a.Nv * a.Cv + (size_t)(t - a.Nv) * a.A);
+  for (int o = 0; o < cout; ++o) {
+    float p = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMaxVpl; ++i)
+      if (i < vpl) p += v[i] * wT[(size_t)o * a.D + lane + kWave * i];
+    p = wave_sum(p);
+    if (lane == 0) {
+      const float vel = p + bias[o];
+      if (a.v_out) a.v_out[base + o] = vel;
+      if (a.x) a.x[base + o] += a.dsigma * vel;
+    }
+  }
+}
+
+// ------------------------------------------------------------- Residual Rescaling
+// Per row: sums of p_i p_a, p_i^2, p_a^2 with p_i = h_s - h_q (float64).
+__global__ void rr_row_sums_kernel(const float* __restrict__ hs, const float* __restrict__ hq,
+                                   const float* __restrict__ pa, double* __restrict__ out,
+                                   int rows, int D) {
+  const int row = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  if (row >= rows) return;
+  const size_t off = (size_t)row * D;
+  double sip = 0.0, sii = 0.0, saa = 0.0;
+  for (int c = lane * 4; c < D; c += kWave * 4) {
+    const float4 s4 = *reinterpret_cast<const float4*>(hs + off + c);
+    const float4 q4 = *reinterpret_cast<const float4*>(hq + off + c);
+    const float4 a4 = *reinterpret_cast<const float4*>(pa + off + c);
+    const float pi[4] = {s4.x - q4.x, s4.y - q4.y, s4.z - q4.z, s4.w - q4.w};
+    const float pv[4] = {a4.x, a4.y, a4.z, a4.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      sip += (double)pi[j] * pv[j];
+      sii += (double)pi[j] * pi[j];
+      saa += (double)pv[j] * pv[j];
+    }
+  }
+  sip = wave_sum_d(sip);
+  sii = wave_sum_d(sii);
+  saa = wave_sum_d(saa);
+  if (lane == 0) {
+    out[(size_t)row * 3 + 0] = sip;
+    out[(size_t)row * 3 + 1] = sii;
+    out[(size_t)row * 3 + 2] = saa;
+  }
+}
+
+// One block per (sample, branch): alpha (Eq. crr-alpha), cos and relative
+// fit error (Eq. crr-gate) from the float64 row sums.
+__global__ void rr_finish_kernel(RRGateArgs a) {
+  const int b = blockIdx.x / 2, br = blockIdx.x % 2;
+  __shared__ double sh[3][16];
+  double s[3] = {0.0, 0.0, 0.0};
+  int nrows;
+  if (br == 1) {
+    nrows = a.Na;
+    for (int t = a.Nv + threadIdx.x; t < a.Nv + a.Na; t += blockDim.x)
+      for (int j = 0; j < 3; ++j) s[j] += a.row_sums[((size_t)b * a.T + t) * 3 + j];
+  } else {
+    nrows = a.T - a.Na;
+    for (int i = threadIdx.x; i < nrows; i += blockDim.x) {
+      const int t = i < a.Nv ? i : i + a.Na;
+      for (int j = 0; j < 3; ++j) s[j] += a.row_sums[((size_t)b * a.T + t) * 3 + j];
+    }
+  }
+  const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  for (int j = 0; j < 3; ++j) {
+    const double v = wave_sum_d(s[j]);
+    if (lane == 0) sh[j][w] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  const int nw = blockDim.x / kWave;
+  double sip = 0.0, sii = 0.0, saa = 0.0;
+  for (int i = 0; i < nw; ++i) {
+    sip += sh[0][i];
+    sii += sh[1][i];
+    saa += sh[2][i];
+  }
+  const double n = (double)nrows * (double)a.D;
+  const double den = fmax(saa / n, (double)a.eps);
+  double alpha = (sip / n) / den;
+  alpha = fmin(fmax(alpha, (double)a.alpha_min), (double)a.alpha_max);
+  const bool ok_norm = sii > 0.0 && saa > 0.0;
+  const double cosv = ok_norm ? sip / sqrt(sii * saa) : 0.0;
+  const double r2 = fmax(sii - 2.0 * alpha * sip + alpha * alpha * saa, 0.0);
+  const double fit = sii > 0.0 ? sqrt(r2) / sqrt(sii) : INFINITY;
+  const bool pass = ok_norm && cosv >= (double)a.gamma_cos && fit <= (double)a.gamma_fit;
+  double* r = a.result + ((size_t)b * 2 + br) * 8;
+  r[0] = sip;
+  r[1] = sii;
+  r[2] = saa;
+  r[3] = alpha;
+  r[4] = cosv;
+  r[5] = fit;
+  r[6] = pass ? 1.0 : 0.0;
+  r[7] = 0.0;
+}
+
+// h_e = h_s + alpha_{b,branch} R_a (Eq. residual-injection), in place on h.
+__global__ void rr_inject_kernel(float* __restrict__ h, const float* __restrict__ Ra,
+                                 const double* __restrict__ result, int rows, int T, int D,
+                                 int Nv, int Na) {
+  const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t n4 = (int64_t)rows * D / 4;
+  if (i4 >= n4) return;
+  const int row = (int)((i4 * 4) / D);
+  const int b = row / T, t = row % T;
+  const int br = (t >= Nv && t < Nv + Na) ? 1 : 0;
+  const float al = (float)result[((size_t)b * 2 + br) * 8 + 3];
+  float4 hv = reinterpret_cast<float4*>(h)[i4];
+  const float4 rv = reinterpret_cast<const float4*>(Ra)[i4];
+  hv.x += al * rv.x;
+  hv.y += al * rv.y;
+  hv.z += al * rv.z;
+  hv.w += al * rv.w;
+  reinterpret_cast<float4*>(h)[i4] = hv;
+}
+
+__global__ void rr_pre_middle_kernel(const float* __restrict__ h, float* __restrict__ hq,
+                                     float* __restrict__ pa, int64_t n4) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  const float4 hv = reinterpret_cast<const float4*>(h)[i];
+  const float4 qv = reinterpret_cast<const float4*>(hq)[i];
+  reinterpret_cast<float4*>(pa)[i] = make_float4(hv.x - qv.x, hv.y - qv.y, hv.z - qv.z, hv.w - qv.w);
+  reinterpret_cast<float4*>(hq)[i] = hv;
+}
+
+__global__ void rr_refresh_kernel(const float* __restrict__ h, const float* __restrict__ hq,
+                                  float* __restrict__ Ra, int64_t n4) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n4) return;
+  const float4 hv = reinterpret_cast<const float4*>(h)[i];
+  const float4 qv = reinterpret_cast<const float4*>(hq)[i];
+  reinterpret_cast<float4*>(Ra)[i] = make_float4(hv.x - qv.x, hv.y - qv.y, hv.z - qv.z, hv.w - qv.w);
+}
+
+// ------------------------------------------------------------- Trajectory Remapping
+// rms of (x^r - x_bar)/sigma_r per (sample, branch) over the whole branch.
+__global__ void remap_rms_kernel(RemapArgs a) {
+  __shared__ double sh[16];
+  const int b = blockIdx.x / 2, br = blockIdx.x % 2;
+  const int traj = a.Nv * a.Cv + a.Na * a.A;
+  const int lo = br == 0 ? 0 : a.Nv * a.Cv;
+  const int hi = br == 0 ? a.Nv * a.Cv : traj;
+  double s = 0.0;
+  for (int i = lo + threadIdx.x; i < hi; i += blockDim.x) {
+    const double d = ((double)a.x_r[(size_t)b * traj + i] - (double)a.x_bar[(size_t)b * traj + i]) /
+                     (double)a.sigma_r;
+    s += d * d;
+  }
+  s = block_sum_d(s, sh);
+  if (threadIdx.x == 0) a.rms[b * 2 + br] = hi > lo ? sqrt(s / (double)(hi - lo)) : 0.0;
+}
+
+// x[j] = x_bar[j+shift] + sigma_b0 d[j+shift] on mapped slots, sigma_b0 eps[j] elsewhere
+__global__ void remap_apply_kernel(RemapArgs a) {
+  const int traj = a.Nv * a.Cv + a.Na * a.A;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)a.B * traj) return;
+  const int b = (int)(idx / traj), i = (int)(idx % traj);
+  const int nv = a.Nv * a.Cv;
+  int br, slot, ch, nslot, width, shift, base;
+  if (i < nv) {
+    br = 0; slot = i / a.Cv; ch = i % a.Cv; nslot = a.Nv; width = a.Cv; shift = a.shift_video; base = 0;
+  } else {
+    br = 1; slot = (i - nv) / a.A; ch = (i - nv) % a.A; nslot = a.Na; width = a.A; shift = a.shift_action; base = nv;
+  }
+  float out;
+  if ((int64_t)slot + shift < nslot) {
+    const size_t src = (size_t)b * traj + base + (size_t)(slot + shift) * width + ch;
+    const double rms = a.rms[b * 2 + br];
+    const double dir = rms > 0.0 ? (((double)a.x_r[src] - (double)a.x_bar[src]) / (double)a.sigma_r) / rms : 0.0;
+    out = (float)((double)a.x_bar[src] + (double)a.sigma_b0 * dir);
+  } else {
+    out = a.sigma_b0 * a.noise[idx];
+  }
+  a.x_out[idx] = out;
+}
+
+// ------------------------------------------------------------- Observation Rebinding
+struct OrSumArgs {
+  const float* u_hat[WAM_MAX_COMPONENTS];
+  const float* u[WAM_MAX_COMPONENTS];
+  int64_t n[WAM_MAX_COMPONENTS];
+  double inv_delta[WAM_MAX_COMPONENTS];
+  double* sums;
+};
+
+__global__ void or_sums_kernel(OrSumArgs a) {
+  __shared__ double sh[16];
+  const int m = blockIdx.x;
+  double s = 0.0;
+  for (int64_t i = threadIdx.x; i < a.n[m]; i += blockDim.x) {
+    const double r = ((double)a.u_hat[m][i] - (double)a.u[m][i]) * a.inv_delta[m];
+    s += r * r;
+  }
+  s = block_sum_d(s, sh);
+  if (threadIdx.x == 0) a.sums[m] = s;
+}
+
+}  // namespace
+
+// ================================================================ launchers
+hipError_t launch_timestep_features(float sigma, float* e, int dim, hipStream_t s) {
+  timestep_features_kernel<<<(dim + 255) / 256, 256, 0, s>>>(sigma, e, dim);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv(const float* x, const void* W, bool w_bf16, const float* b, float* y,
+                       float* partial, int K, int N, int in_act, int out_act, hipStream_t s) {
+  if (N % kGemvVec) return hipErrorInvalidValue;
+  const int nchunk = (K + kGemvKc - 1) / kGemvKc;
+  dim3 grid((N / kGemvVec + 255) / 256, nchunk);
+  if (w_bf16)
+    gemv_partial_kernel<bf16><<<grid, 256, 0, s>>>(x, (const bf16*)W, partial, K, N, in_act);
+  else
+    gemv_partial_kernel<float><<<grid, 256, 0, s>>>(x, (const float*)W, partial, K, N, in_act);
+  gemv_reduce_kernel<<<(N + 255) / 256, 256, 0, s>>>(partial, b, y, nchunk, N, out_act);
+  return hipGetLastError();
+}
+
+hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
+  if (a.Cv > 64 || a.A > 64 || a.Co > 64) return hipErrorInvalidValue;
+  embed_kernel<<<a.B * a.T, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_modulate(const float* h, const float* shift, const float* scale, void* u,
+                              int rows, int D, float eps, bool bf16_out, hipStream_t s) {
+  if (D % kWave || D / kWave > kMaxVpl) return hipErrorInvalidValue;
+  const int wpb = 4;
+  dim3 grid((rows + wpb - 1) / wpb);
+  if (bf16_out)
+    ln_modulate_kernel<bf16><<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (bf16*)u, rows, D, eps);
+  else
+    ln_modulate_kernel<float><<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (float*)u, rows, D, eps);
+  return hipGetLastError();
+}
+
+hipError_t launch_final(const FinalArgs& a, hipStream_t s) {
+  if (a.D % kWave || a.D / kWave > kMaxVpl) return hipErrorInvalidValue;
+  const int wpb = 4;
+  const int rows = a.B * (a.Nv + a.Na);
+  final_kernel<<<(rows + wpb - 1) / wpb, wpb * kWave, 0, s>>>(a, a.wv, a.wa);
+  return hipGetLastError();
+}
+
+hipError_t launch_rr_gate(const RRGateArgs& a, hipStream_t s) {
+  const int rows = a.B * a.T;
+  if (a.D % 4) return hipErrorInvalidValue;
+  const int wpb = 4;
+  rr_row_sums_kernel<<<(rows + wpb - 1) / wpb, wpb * kWave, 0, s>>>(a.hs, a.hq, a.pa, a.row_sums, rows, a.D);
+  rr_finish_kernel<<<a.B * 2, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_rr_inject(float* h, const float* Ra, const double* result, int B, int T, int D,
+                            int Nv, int Na, hipStream_t s) {
+  const int64_t n4 = (int64_t)B * T * D / 4;
+  rr_inject_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(h, Ra, result, B * T, T, D, Nv, Na);
+  return hipGetLastError();
+}
+
+hipError_t launch_rr_pre_middle(const float* h, float* hq, float* pa, int64_t n, hipStream_t s) {
+  const int64_t n4 = n / 4;
+  rr_pre_middle_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(h, hq, pa, n4);
+  return hipGetLastError();
+}
+
+hipError_t launch_rr_refresh(const float* h, const float* hq, float* Ra, int64_t n, hipStream_t s) {
+  const int64_t n4 = n / 4;
+  rr_refresh_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(h, hq, Ra, n4);
+  return hipGetLastError();
+}
+
+hipError_t launch_remap(const RemapArgs& a, hipStream_t s) {
+  remap_rms_kernel<<<a.B * 2, 256, 0, s>>>(a);
+  const int64_t n = (int64_t)a.B * (a.Nv * a.Cv + a.Na * a.A);
+  remap_apply_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_or_sums(int n_comp, const float* const* u_hat, const float* const* u,
+                          const int64_t* n, const double* delta, double* sums, hipStream_t s) {
+  if (n_comp < 1 || n_comp > WAM_MAX_COMPONENTS) return hipErrorInvalidValue;
+  OrSumArgs a{};
+  for (int m = 0; m < n_comp; ++m) {
+    a.u_hat[m] = u_hat[m];
+    a.u[m] = u[m];
+    a.n[m] = n[m];
+    a.inv_delta[m] = 1.0 / delta[m];
+  }
+  a.sums = sums;
+  or_sums_kernel<<<n_comp, 256, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace wam

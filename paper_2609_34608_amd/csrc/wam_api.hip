@@ -1,0 +1,894 @@
+// libwam C ABI: handle, validation, weight packing, workspace carving, the
+// denoising-step driver and the joint replan runtime (host side).
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "wam_internal.h"
+
+using namespace wam;
+
+namespace {
+
+constexpr int kTimeDim = 256;
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+uint16_t f32_to_bf16_bits(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffff) ? 0x40 : 0));
+  const uint32_t lsb = (u >> 16) & 1u;
+  u += 0x7fffu + lsb;
+  return (uint16_t)(u >> 16);
+}
+
+struct Dims {
+  int B, L, D, H, F, Nv, Cv, Na, A, No, Co, T, M, dh, Tpad, traj, Nmod;
+  bool bf;
+  size_t act;  // bytes per activation element
+};
+
+int make_dims(const wam_config* c, Dims* d, std::string* why) {
+  auto bad = [&](const char* m) {
+    if (why) *why = m;
+    return WAM_E_SHAPE;
+  };
+  if (!c) {
+    if (why) *why = "null config";
+    return WAM_E_ARG;
+  }
+  if (c->B < 1 || c->B > WAM_MAX_BATCH) return bad("B must be in 1..WAM_MAX_BATCH");
+  if (c->L < 1 || c->D < 64 || c->H < 1 || c->F < 64) return bad("L, D, H, F out of range");
+  if (c->Nv < 0 || c->Na < 1 || c->No < 0 || c->Cv < 1 || c->A < 1 || c->Co < 1)
+    return bad("token counts / channels out of range");
+  if (c->Cv > 64 || c->A > 64 || c->Co > 64) return bad("Cv, A, Co must be <= 64");
+  if (c->D % c->H) return bad("D must be divisible by H");
+  if (c->D % 64 || c->D > 2048) return bad("D must be a multiple of 64 and <= 2048");
+  if (c->dtype != WAM_FP32 && c->dtype != WAM_BF16) return bad("dtype must be WAM_FP32 or WAM_BF16");
+  const int dh = c->D / c->H;
+  if (dh != 32 && dh != 64) return bad("head size D/H must be 32 or 64");
+  if (c->dtype == WAM_BF16) {
+    if (dh != 64) return bad("bf16 mode needs head size 64");
+    if (c->D % 128 || c->F % 128) return bad("bf16 mode needs D and F multiples of 128");
+  } else {
+    if (c->F % 64) return bad("F must be a multiple of 64");
+  }
+  if (!(c->ln_eps > 0.f)) return bad("ln_eps must be > 0");
+  d->B = c->B; d->L = c->L; d->D = c->D; d->H = c->H; d->F = c->F;
+  d->Nv = c->Nv; d->Cv = c->Cv; d->Na = c->Na; d->A = c->A; d->No = c->No; d->Co = c->Co;
+  d->T = c->Nv + c->Na + c->No;
+  d->M = d->B * d->T;
+  d->dh = dh;
+  d->Tpad = (d->T + 63) / 64 * 64;
+  d->traj = c->Nv * c->Cv + c->Na * c->A;
+  d->Nmod = c->L * 6 * c->D + 2 * c->D;
+  d->bf = c->dtype == WAM_BF16;
+  d->act = d->bf ? 2 : 4;
+  return WAM_OK;
+}
+
+// ---- canonical host weight layout (see wam.h)
+struct HostLayout {
+  size_t t_w1, t_b1, t_w2, t_b2, in_wv, in_bv, in_wa, in_ba, in_wo, in_bo;
+  size_t layer0, layer_stride;
+  size_t mod_w, mod_b, qkv_w, qkv_b, q_g, k_g, proj_w, proj_b, fc1_w, fc1_b, fc2_w, fc2_b;  // in layer
+  size_t f_mod_w, f_mod_b, out_wv, out_bv, out_wa, out_ba, total;
+};
+
+HostLayout host_layout(const Dims& d) {
+  HostLayout h{};
+  size_t o = 0;
+  auto take = [&](size_t n) {
+    size_t r = o;
+    o += n;
+    return r;
+  };
+  const size_t D = d.D, F = d.F;
+  h.t_w1 = take(kTimeDim * D); h.t_b1 = take(D); h.t_w2 = take(D * D); h.t_b2 = take(D);
+  h.in_wv = take((size_t)d.Cv * D); h.in_bv = take(D);
+  h.in_wa = take((size_t)d.A * D); h.in_ba = take(D);
+  h.in_wo = take((size_t)d.Co * D); h.in_bo = take(D);
+  h.layer0 = o;
+  size_t l = 0;
+  auto ltake = [&](size_t n) {
+    size_t r = l;
+    l += n;
+    return r;
+  };
+  h.mod_w = ltake(D * 6 * D); h.mod_b = ltake(6 * D);
+  h.qkv_w = ltake(D * 3 * D); h.qkv_b = ltake(3 * D);
+  h.q_g = ltake(d.dh); h.k_g = ltake(d.dh);
+  h.proj_w = ltake(D * D); h.proj_b = ltake(D);
+  h.fc1_w = ltake(D * F); h.fc1_b = ltake(F);
+  h.fc2_w = ltake(F * D); h.fc2_b = ltake(D);
+  h.layer_stride = l;
+  o += l * d.L;
+  h.f_mod_w = take(D * 2 * D); h.f_mod_b = take(2 * D);
+  h.out_wv = take(D * d.Cv); h.out_bv = take(d.Cv);
+  h.out_wa = take(D * d.A); h.out_ba = take(d.A);
+  h.total = o;
+  return h;
+}
+
+// ---- device weight layout
+struct DevLayout {
+  // float32 region
+  size_t t_w1, t_b1, t_w2, t_b2, in_wv, in_bv, in_wa, in_ba, in_wo, in_bo;
+  size_t bmod;                        // [Nmod] all layers' mod_b then f_mod_b
+  size_t lbias0, lbias_stride;        // per layer: qkv_b, proj_b, fc1_b, fc2_b, q_g, k_g
+  size_t out_wvT, out_bv, out_waT, out_ba;
+  // activation-typed region
+  size_t wmod;                        // [D][Nmod]
+  size_t lw0, lw_stride;              // per layer: qkv_wT [3D][D], proj_wT [D][D], fc1_wT [F][D], fc2_wT [D][F]
+  size_t total;
+};
+
+DevLayout dev_layout(const Dims& d) {
+  DevLayout w{};
+  size_t o = 0;
+  auto f32 = [&](size_t n) {
+    size_t r = o;
+    o = align_up(o + n * 4);
+    return r;
+  };
+  const size_t D = d.D, F = d.F;
+  w.t_w1 = f32(kTimeDim * D); w.t_b1 = f32(D); w.t_w2 = f32(D * D); w.t_b2 = f32(D);
+  w.in_wv = f32((size_t)d.Cv * D); w.in_bv = f32(D);
+  w.in_wa = f32((size_t)d.A * D); w.in_ba = f32(D);
+  w.in_wo = f32((size_t)d.Co * D); w.in_bo = f32(D);
+  w.bmod = f32(d.Nmod);
+  w.lbias_stride = align_up((3 * D + D + F + D + 2 * d.dh) * 4);
+  w.lbias0 = o;
+  o += w.lbias_stride * d.L;
+  w.out_wvT = f32(D * d.Cv); w.out_bv = f32(d.Cv);
+  w.out_waT = f32(D * d.A); w.out_ba = f32(d.A);
+  w.wmod = o;
+  o = align_up(o + D * d.Nmod * d.act);
+  w.lw_stride = align_up((3 * D * D + D * D + F * D + D * F) * d.act);
+  w.lw0 = o;
+  o += w.lw_stride * d.L;
+  w.total = o;
+  return w;
+}
+
+struct WsLayout {
+  size_t h, hq, pa, Ra, u, qkv, q, k, vt, attn, mlp, e, a1, sc, mod, gpart, v;
+  size_t x_bar, x_r, x_init, x_work, rr_rows, rr_res, tr_rms, or_sums, total;
+  size_t gpart_floats;
+};
+
+WsLayout ws_layout(const Dims& d) {
+  WsLayout w{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t r = o;
+    o = align_up(o + bytes);
+    return r;
+  };
+  const size_t MD = (size_t)d.M * d.D;
+  w.h = take(MD * 4); w.hq = take(MD * 4); w.pa = take(MD * 4); w.Ra = take(MD * 4);
+  w.u = take(MD * d.act);
+  w.qkv = take(MD * 3 * d.act);
+  const size_t head = (size_t)d.B * d.H * d.Tpad * d.dh;
+  w.q = take(head * d.act); w.k = take(head * d.act); w.vt = take(head * d.act);
+  w.attn = take(MD * d.act);
+  w.mlp = take((size_t)d.M * d.F * d.act);
+  w.e = take(kTimeDim * 4); w.a1 = take(d.D * 4); w.sc = take(d.D * 4);
+  w.mod = take((size_t)d.Nmod * 4);
+  const size_t kmax = std::max(d.D, kTimeDim);
+  const size_t nmax = std::max<size_t>(d.Nmod, d.D);
+  w.gpart_floats = ((kmax + 31) / 32) * nmax;
+  w.gpart = take(w.gpart_floats * 4);
+  const size_t tr = (size_t)d.B * d.traj * 4;
+  w.v = take(tr); w.x_bar = take(tr); w.x_r = take(tr); w.x_init = take(tr); w.x_work = take(tr);
+  w.rr_rows = take((size_t)d.M * 3 * 8);
+  w.rr_res = take((size_t)d.B * 2 * 8 * 8);
+  w.tr_rms = take((size_t)d.B * 2 * 8);
+  w.or_sums = take(WAM_MAX_COMPONENTS * 8);
+  w.total = o;
+  return w;
+}
+
+struct ProfSlot {
+  bool on = false;
+  int max = 0;
+  int used = 0;
+  std::vector<hipEvent_t> ev;  // 2 per launch
+  std::vector<double> work;
+};
+
+}  // namespace
+
+struct wam_handle {
+  wam_config cfg;
+  Dims d;
+  DevLayout wl;
+  WsLayout ws;
+  char* wdev = nullptr;
+  char* wsdev = nullptr;
+  hipStream_t stream = nullptr;
+  std::vector<float> sigmas;
+  int K = 0;
+  bool layer_valid = false;
+  bool has_prev = false;
+  int kappa = 0;
+  double* host_stage = nullptr;  // pinned, small
+  std::string err;
+  ProfSlot prof[WAM_KC_COUNT];
+
+  template <typename T = float>
+  T* W(size_t off) const { return reinterpret_cast<T*>(wdev + off); }
+  template <typename T = float>
+  T* S(size_t off) const { return reinterpret_cast<T*>(wsdev + off); }
+};
+
+namespace {
+
+int fail(wam_t h, int code, const std::string& msg) {
+  if (h) h->err = msg;
+  return code;
+}
+
+#define HIPCHK(h, expr)                                                               \
+  do {                                                                                \
+    hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess)                                                             \
+      return fail(h, WAM_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_));   \
+  } while (0)
+
+// ---- per-launch timing for the measurement API
+struct ProfScope {
+  wam_t h;
+  int kc;
+  bool on;
+  ProfScope(wam_t h_, int kc_, double work) : h(h_), kc(kc_), on(false) {
+    ProfSlot& p = h->prof[kc];
+    if (p.on && p.used < p.max) {
+      on = true;
+      hipEventRecord(p.ev[2 * p.used], h->stream);
+      p.work[p.used] = work;
+    }
+  }
+  ~ProfScope() {
+    if (on) {
+      ProfSlot& p = h->prof[kc];
+      hipEventRecord(p.ev[2 * p.used + 1], h->stream);
+      ++p.used;
+    }
+  }
+};
+
+// ---- step pieces
+int compute_conditioning(wam_t h, float sigma) {
+  const Dims& d = h->d;
+  const DevLayout& wl = h->wl;
+  const WsLayout& ws = h->ws;
+  hipStream_t s = h->stream;
+  HIPCHK(h, launch_timestep_features(sigma, h->S(ws.e), kTimeDim, s));
+  HIPCHK(h, launch_gemv(h->S(ws.e), h->W(wl.t_w1), false, h->W(wl.t_b1), h->S(ws.a1), h->S(ws.gpart),
+                        kTimeDim, d.D, 0, 1, s));
+  HIPCHK(h, launch_gemv(h->S(ws.a1), h->W(wl.t_w2), false, h->W(wl.t_b2), h->S(ws.sc), h->S(ws.gpart),
+                        d.D, d.D, 0, 1, s));
+  // sc now holds SiLU(c); all adaLN modulations in one pass
+  HIPCHK(h, launch_gemv(h->S(ws.sc), h->W<char>(wl.wmod), d.bf, h->W(wl.bmod), h->S(ws.mod),
+                        h->S(ws.gpart), d.D, d.Nmod, 0, 0, s));
+  return WAM_OK;
+}
+
+int embed(wam_t h, const float* x, const float* cond) {
+  const Dims& d = h->d;
+  const DevLayout& wl = h->wl;
+  EmbedArgs a{};
+  a.x = x; a.cond = cond;
+  a.wv = h->W(wl.in_wv); a.bv = h->W(wl.in_bv);
+  a.wa = h->W(wl.in_wa); a.ba = h->W(wl.in_ba);
+  a.wo = h->W(wl.in_wo); a.bo = h->W(wl.in_bo);
+  a.h = h->S(h->ws.h);
+  a.B = d.B; a.T = d.T; a.D = d.D; a.Nv = d.Nv; a.Cv = d.Cv; a.Na = d.Na; a.A = d.A; a.No = d.No; a.Co = d.Co;
+  HIPCHK(h, launch_embed(a, h->stream));
+  return WAM_OK;
+}
+
+int run_layer(wam_t h, int l) {
+  const Dims& d = h->d;
+  const DevLayout& wl = h->wl;
+  const WsLayout& ws = h->ws;
+  hipStream_t s = h->stream;
+  const size_t D = d.D;
+  const float* mod = h->S(ws.mod) + (size_t)l * 6 * D;
+  const float* lb = h->W(wl.lbias0 + wl.lbias_stride * l);
+  const float* qkv_b = lb;
+  const float* proj_b = lb + 3 * D;
+  const float* fc1_b = proj_b + D;
+  const float* fc2_b = fc1_b + d.F;
+  const float* q_g = fc2_b + D;
+  const float* k_g = q_g + d.dh;
+  const char* lw = h->W<char>(wl.lw0 + wl.lw_stride * l);
+  const char* qkv_w = lw;
+  const char* proj_w = qkv_w + 3 * D * D * d.act;
+  const char* fc1_w = proj_w + D * D * d.act;
+  const char* fc2_w = fc1_w + (size_t)d.F * D * d.act;
+  float* hh = h->S(ws.h);
+  const double M = d.M;
+
+  HIPCHK(h, launch_ln_modulate(hh, mod + 0 * D, mod + 1 * D, h->S<char>(ws.u), d.M, d.D, h->cfg.ln_eps, d.bf, s));
+  {
+    ProfScope ps(h, WAM_KC_GEMM_QKV, 2.0 * M * D * 3 * D);
+    GemmArgs g{h->S<char>(ws.u), qkv_w, qkv_b, nullptr, h->S<char>(ws.qkv), d.M, (int)(3 * D), (int)D, EPI_BIAS};
+    HIPCHK(h, launch_gemm(g, d.bf, s));
+  }
+  {
+    RelayoutArgs r{h->S<char>(ws.qkv), q_g, k_g, h->S<char>(ws.q), h->S<char>(ws.k), h->S<char>(ws.vt),
+                   d.B, d.H, d.T, d.Tpad, d.dh, d.D, h->cfg.qk_norm, h->cfg.ln_eps};
+    HIPCHK(h, launch_qkv_relayout(r, d.bf, s));
+  }
+  {
+    ProfScope ps(h, WAM_KC_ATTENTION, 4.0 * d.B * (double)d.T * d.T * D);
+    AttnArgs at{h->S<char>(ws.q), h->S<char>(ws.k), h->S<char>(ws.vt), h->S<char>(ws.attn),
+                d.B, d.H, d.T, d.Tpad, d.dh, d.D};
+    HIPCHK(h, launch_attention(at, d.bf, s));
+  }
+  {
+    ProfScope ps(h, WAM_KC_GEMM_PROJ, 2.0 * M * D * D);
+    GemmArgs g{h->S<char>(ws.attn), proj_w, proj_b, mod + 2 * D, hh, d.M, (int)D, (int)D, EPI_GATED_RES};
+    HIPCHK(h, launch_gemm(g, d.bf, s));
+  }
+  HIPCHK(h, launch_ln_modulate(hh, mod + 3 * D, mod + 4 * D, h->S<char>(ws.u), d.M, d.D, h->cfg.ln_eps, d.bf, s));
+  {
+    ProfScope ps(h, WAM_KC_GEMM_FC1, 2.0 * M * D * d.F);
+    GemmArgs g{h->S<char>(ws.u), fc1_w, fc1_b, nullptr, h->S<char>(ws.mlp), d.M, d.F, (int)D, EPI_BIAS_GELU};
+    HIPCHK(h, launch_gemm(g, d.bf, s));
+  }
+  {
+    ProfScope ps(h, WAM_KC_GEMM_FC2, 2.0 * M * D * d.F);
+    GemmArgs g{h->S<char>(ws.mlp), fc2_w, fc2_b, mod + 5 * D, hh, d.M, (int)D, d.F, EPI_GATED_RES};
+    HIPCHK(h, launch_gemm(g, d.bf, s));
+  }
+  return WAM_OK;
+}
+
+int run_layers(wam_t h, int lo, int hi) {
+  for (int l = lo; l < hi; ++l) {
+    int st = run_layer(h, l);
+    if (st) return st;
+  }
+  return WAM_OK;
+}
+
+int check_rr(wam_t h, const wam_rr_profile* rr) {
+  if (!rr || rr->mode == WAM_RR_OFF) return WAM_OK;
+  if (rr->mode < 0 || rr->mode > WAM_RR_FORCE_FULL) return fail(h, WAM_E_ARG, "unknown RR mode");
+  if (!(0 < rr->q && rr->q < rr->s && rr->s < rr->e && rr->e < h->d.L))
+    return fail(h, WAM_E_ARG, "RR needs 0 < q < s < e < L");
+  if (!(rr->alpha_min <= rr->alpha_max) || !(rr->eps > 0.f))
+    return fail(h, WAM_E_ARG, "RR needs alpha_min <= alpha_max and eps > 0");
+  return WAM_OK;
+}
+
+// Full forward with Residual Rescaling, then the final layer (velocity into
+// v_out and/or Euler update of x by dsigma).
+int forward(wam_t h, int k, const float* x, const float* cond, float* v_out, float* x_euler,
+            const wam_rr_profile* rr, wam_step_info* info) {
+  const Dims& d = h->d;
+  const WsLayout& ws = h->ws;
+  hipStream_t s = h->stream;
+  wam_step_info local{};
+  wam_step_info* in = info ? info : &local;
+  memset(in, 0, sizeof(*in));
+  in->layers_evaluated = d.L;
+  int st = compute_conditioning(h, h->sigmas[k]);
+  if (st) return st;
+  if ((st = embed(h, x, cond))) return st;
+  const bool active = rr && rr->mode != WAM_RR_OFF;
+  float* hh = h->S(ws.h);
+  const int64_t MD = (int64_t)d.M * d.D;
+  if (!active) {
+    if ((st = run_layers(h, 0, d.L))) return st;
+  } else {
+    in->rr_active = 1;
+    if ((st = run_layers(h, 0, rr->q))) return st;
+    HIPCHK(h, hipMemcpyAsync(h->S(ws.hq), hh, MD * 4, hipMemcpyDeviceToDevice, s));
+    if ((st = run_layers(h, rr->q, rr->s))) return st;
+    bool accept = false;
+    if (h->layer_valid && (rr->mode == WAM_RR_AUTO || rr->mode == WAM_RR_FORCE_SKIP)) {
+      in->rr_attempted = 1;
+      RRGateArgs g{hh, h->S(ws.hq), h->S(ws.pa), h->S<double>(ws.rr_rows), h->S<double>(ws.rr_res),
+                   d.B, d.T, d.D, d.Nv, d.Na, rr->alpha_min, rr->alpha_max, rr->eps, rr->gamma_cos,
+                   rr->gamma_fit};
+      {
+        ProfScope ps(h, WAM_KC_RR_GATE, 3.0 * MD * 4);
+        HIPCHK(h, launch_rr_gate(g, s));
+      }
+      const size_t nres = (size_t)d.B * 2 * 8;
+      HIPCHK(h, hipMemcpyAsync(h->host_stage, h->S<double>(ws.rr_res), nres * 8, hipMemcpyDeviceToHost, s));
+      HIPCHK(h, hipStreamSynchronize(s));
+      bool all = true;
+      for (int b = 0; b < d.B; ++b)
+        for (int br = 0; br < 2; ++br) {
+          const double* r = h->host_stage + ((size_t)b * 2 + br) * 8;
+          in->alpha[b][br] = r[3];
+          in->cos[b][br] = r[4];
+          in->fit[b][br] = r[5];
+          all = all && r[6] != 0.0;
+        }
+      accept = rr->mode == WAM_RR_FORCE_SKIP ? true : all;
+    }
+    if (accept) {
+      ProfScope ps(h, WAM_KC_RR_INJECT, 3.0 * MD * 4);
+      HIPCHK(h, launch_rr_inject(hh, h->S(ws.Ra), h->S<double>(ws.rr_res), d.B, d.T, d.D, d.Nv, d.Na, s));
+      in->rr_accepted = 1;
+      in->layers_skipped = rr->e - rr->s;
+      in->layers_evaluated = d.L - (rr->e - rr->s);
+    } else {
+      HIPCHK(h, launch_rr_pre_middle(hh, h->S(ws.hq), h->S(ws.pa), MD, s));
+      if ((st = run_layers(h, rr->s, rr->e))) return st;
+      {
+        ProfScope ps(h, WAM_KC_RR_REFRESH, 3.0 * MD * 4);
+        HIPCHK(h, launch_rr_refresh(hh, h->S(ws.hq), h->S(ws.Ra), MD, s));
+      }
+      h->layer_valid = true;
+    }
+    if ((st = run_layers(h, rr->e, d.L))) return st;
+  }
+  FinalArgs f{};
+  const float* fm = h->S(ws.mod) + (size_t)d.L * 6 * d.D;
+  f.h = hh; f.shift = fm; f.scale = fm + d.D;
+  f.wv = h->W(h->wl.out_wvT); f.bv = h->W(h->wl.out_bv);
+  f.wa = h->W(h->wl.out_waT); f.ba = h->W(h->wl.out_ba);
+  f.v_out = v_out; f.x = x_euler;
+  f.dsigma = (k + 1 <= h->K) ? h->sigmas[k + 1] - h->sigmas[k] : 0.f;
+  f.B = d.B; f.T = d.T; f.D = d.D; f.Nv = d.Nv; f.Cv = d.Cv; f.Na = d.Na; f.A = d.A; f.eps = h->cfg.ln_eps;
+  HIPCHK(h, launch_final(f, s));
+  return WAM_OK;
+}
+
+int check_step(wam_t h, int k, const void* x, const void* cond) {
+  if (!h) return WAM_E_ARG;
+  if (h->K <= 0) return fail(h, WAM_E_STATE, "schedule not set (wam_set_schedule)");
+  if (k < 0 || k >= h->K) return fail(h, WAM_E_ARG, "step index out of range");
+  if (!x || !cond) return fail(h, WAM_E_ARG, "null trajectory or condition pointer");
+  return WAM_OK;
+}
+
+int copy_traj(wam_t h, float* dst, const float* src) {
+  HIPCHK(h, hipMemcpyAsync(dst, src, (size_t)h->d.B * h->d.traj * 4, hipMemcpyDeviceToDevice, h->stream));
+  return WAM_OK;
+}
+
+int continue_impl(wam_t h, int k_from, int k_to, float* x, const float* cond, const wam_rr_profile* rr,
+                  int capture_stage, float* x_capture, wam_step_info* infos) {
+  for (int k = k_from; k < k_to; ++k) {
+    if (capture_stage == k && x_capture) {
+      int st = copy_traj(h, x_capture, x);
+      if (st) return st;
+    }
+    int st = forward(h, k, x, cond, nullptr, x, rr, infos ? &infos[k - k_from] : nullptr);
+    if (st) return st;
+  }
+  if (capture_stage == k_to && x_capture) return copy_traj(h, x_capture, x);
+  return WAM_OK;
+}
+
+}  // namespace
+
+// =====================================================================
+extern "C" {
+
+const char* wam_status_string(int s) {
+  switch (s) {
+    case WAM_OK: return "ok";
+    case WAM_E_ARG: return "invalid argument";
+    case WAM_E_SHAPE: return "unsupported or mismatched shape";
+    case WAM_E_STATE: return "invalid state for this call";
+    case WAM_E_HIP: return "HIP runtime error";
+    case WAM_E_WORKSPACE: return "buffer too small";
+    case WAM_E_UNSUPPORTED: return "unsupported";
+    default: return "unknown status";
+  }
+}
+
+size_t wam_host_weight_count(const wam_config* cfg) {
+  Dims d;
+  if (make_dims(cfg, &d, nullptr)) return 0;
+  return host_layout(d).total;
+}
+
+size_t wam_weight_bytes(const wam_config* cfg) {
+  Dims d;
+  if (make_dims(cfg, &d, nullptr)) return 0;
+  return dev_layout(d).total;
+}
+
+size_t wam_workspace_bytes(const wam_config* cfg) {
+  Dims d;
+  if (make_dims(cfg, &d, nullptr)) return 0;
+  return ws_layout(d).total;
+}
+
+int64_t wam_traj_elems(const wam_config* cfg) {
+  Dims d;
+  if (make_dims(cfg, &d, nullptr)) return 0;
+  return d.traj;
+}
+
+int wam_init(const wam_config* cfg, const float* hw, size_t n_hw, void* dev_weights, size_t weight_bytes,
+             void* dev_ws, size_t ws_bytes, void* stream, wam_t* out) {
+  if (!out) return WAM_E_ARG;
+  *out = nullptr;
+  Dims d;
+  std::string why;
+  int st = make_dims(cfg, &d, &why);
+  if (st) {
+    fprintf(stderr, "wam_init: %s\n", why.c_str());
+    return st;
+  }
+  if (!hw || !dev_weights || !dev_ws) return WAM_E_ARG;
+  const HostLayout hl = host_layout(d);
+  if (n_hw != hl.total) return WAM_E_SHAPE;
+  const DevLayout wl = dev_layout(d);
+  const WsLayout ws = ws_layout(d);
+  if (weight_bytes < wl.total || ws_bytes < ws.total) return WAM_E_WORKSPACE;
+
+  wam_handle* h = new wam_handle();
+  h->cfg = *cfg;
+  h->d = d;
+  h->wl = wl;
+  h->ws = ws;
+  h->wdev = static_cast<char*>(dev_weights);
+  h->wsdev = static_cast<char*>(dev_ws);
+  h->stream = static_cast<hipStream_t>(stream);
+  if (hipHostMalloc((void**)&h->host_stage, 4096, hipHostMallocDefault) != hipSuccess) {
+    delete h;
+    return WAM_E_HIP;
+  }
+
+  // ---- pack weights on the host, then one copy
+  std::vector<char> buf(wl.total, 0);
+  auto f32 = [&](size_t dst, size_t src, size_t n) { memcpy(buf.data() + dst, hw + src, n * 4); };
+  const size_t D = d.D, F = d.F;
+  f32(wl.t_w1, hl.t_w1, kTimeDim * D); f32(wl.t_b1, hl.t_b1, D);
+  f32(wl.t_w2, hl.t_w2, D * D); f32(wl.t_b2, hl.t_b2, D);
+  f32(wl.in_wv, hl.in_wv, d.Cv * D); f32(wl.in_bv, hl.in_bv, D);
+  f32(wl.in_wa, hl.in_wa, d.A * D); f32(wl.in_ba, hl.in_ba, D);
+  f32(wl.in_wo, hl.in_wo, d.Co * D); f32(wl.in_bo, hl.in_bo, D);
+  auto put_act = [&](size_t dst_off, size_t idx, float v) {
+    if (d.bf) {
+      uint16_t b = f32_to_bf16_bits(v);
+      memcpy(buf.data() + dst_off + idx * 2, &b, 2);
+    } else {
+      memcpy(buf.data() + dst_off + idx * 4, &v, 4);
+    }
+  };
+  // transposed copy: src [rows][cols] -> dst [cols][rows]
+  auto put_T = [&](size_t dst_off, const float* src, size_t rows, size_t cols) {
+    const size_t tb = 64;
+    for (size_t r0 = 0; r0 < rows; r0 += tb)
+      for (size_t c0 = 0; c0 < cols; c0 += tb)
+        for (size_t r = r0; r < std::min(rows, r0 + tb); ++r)
+          for (size_t c = c0; c < std::min(cols, c0 + tb); ++c) put_act(dst_off, c * rows + r, src[r * cols + c]);
+  };
+  for (int l = 0; l < d.L; ++l) {
+    const float* L0 = hw + hl.layer0 + hl.layer_stride * l;
+    // modulation: rows k of [D][6D] into the shared [D][Nmod] matrix
+    for (size_t r = 0; r < D; ++r)
+      for (size_t c = 0; c < 6 * D; ++c) put_act(wl.wmod, r * d.Nmod + (size_t)l * 6 * D + c, L0[hl.mod_w + r * 6 * D + c]);
+    memcpy(buf.data() + wl.bmod + (size_t)l * 6 * D * 4, L0 + hl.mod_b, 6 * D * 4);
+    const size_t lb = wl.lbias0 + wl.lbias_stride * l;
+    memcpy(buf.data() + lb, L0 + hl.qkv_b, 3 * D * 4);
+    memcpy(buf.data() + lb + 3 * D * 4, L0 + hl.proj_b, D * 4);
+    memcpy(buf.data() + lb + 4 * D * 4, L0 + hl.fc1_b, F * 4);
+    memcpy(buf.data() + lb + (4 * D + F) * 4, L0 + hl.fc2_b, D * 4);
+    memcpy(buf.data() + lb + (5 * D + F) * 4, L0 + hl.q_g, d.dh * 4);
+    memcpy(buf.data() + lb + (5 * D + F + d.dh) * 4, L0 + hl.k_g, d.dh * 4);
+    const size_t lw = wl.lw0 + wl.lw_stride * l;
+    put_T(lw, L0 + hl.qkv_w, D, 3 * D);
+    put_T(lw + 3 * D * D * d.act, L0 + hl.proj_w, D, D);
+    put_T(lw + 4 * D * D * d.act, L0 + hl.fc1_w, D, F);
+    put_T(lw + (4 * D * D + F * D) * d.act, L0 + hl.fc2_w, F, D);
+  }
+  for (size_t r = 0; r < D; ++r)
+    for (size_t c = 0; c < 2 * D; ++c)
+      put_act(wl.wmod, r * d.Nmod + (size_t)d.L * 6 * D + c, hw[hl.f_mod_w + r * 2 * D + c]);
+  memcpy(buf.data() + wl.bmod + (size_t)d.L * 6 * D * 4, hw + hl.f_mod_b, 2 * D * 4);
+  {
+    float* wvT = reinterpret_cast<float*>(buf.data() + wl.out_wvT);
+    for (size_t r = 0; r < D; ++r)
+      for (int c = 0; c < d.Cv; ++c) wvT[(size_t)c * D + r] = hw[hl.out_wv + r * d.Cv + c];
+    float* waT = reinterpret_cast<float*>(buf.data() + wl.out_waT);
+    for (size_t r = 0; r < D; ++r)
+      for (int c = 0; c < d.A; ++c) waT[(size_t)c * D + r] = hw[hl.out_wa + r * d.A + c];
+  }
+  f32(wl.out_bv, hl.out_bv, d.Cv);
+  f32(wl.out_ba, hl.out_ba, d.A);
+  hipError_t e = hipMemcpy(h->wdev, buf.data(), wl.total, hipMemcpyHostToDevice);
+  // pads of q/k/v^T beyond T are read by the attention tiles and must be zero
+  if (e == hipSuccess) e = hipMemsetAsync(h->wsdev + ws.q, 0, ws.attn - ws.q, h->stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
+  if (e != hipSuccess) {
+    fprintf(stderr, "wam_init: %s\n", hipGetErrorString(e));
+    hipHostFree(h->host_stage);
+    delete h;
+    return WAM_E_HIP;
+  }
+  *out = h;
+  return WAM_OK;
+}
+
+void wam_destroy(wam_t h) {
+  if (!h) return;
+  for (auto& p : h->prof)
+    for (auto ev : p.ev) hipEventDestroy(ev);
+  if (h->host_stage) hipHostFree(h->host_stage);
+  delete h;
+}
+
+int wam_sync(wam_t h) {
+  if (!h) return WAM_E_ARG;
+  HIPCHK(h, hipStreamSynchronize(h->stream));
+  return WAM_OK;
+}
+
+const char* wam_last_error(wam_t h) { return h ? h->err.c_str() : "null handle"; }
+
+int wam_set_schedule(wam_t h, const float* sigmas, int K) {
+  if (!h) return WAM_E_ARG;
+  if (!sigmas || K < 1 || K > WAM_MAX_STEPS) return fail(h, WAM_E_ARG, "need 1 <= K <= WAM_MAX_STEPS");
+  for (int i = 0; i < K; ++i)
+    if (!(sigmas[i + 1] < sigmas[i])) return fail(h, WAM_E_ARG, "sigmas must decrease strictly");
+  h->sigmas.assign(sigmas, sigmas + K + 1);
+  h->K = K;
+  return WAM_OK;
+}
+
+int wam_velocity(wam_t h, int k, const float* x, const float* cond, float* v_out, const wam_rr_profile* rr,
+                 wam_step_info* info) {
+  int st = check_step(h, k, x, cond);
+  if (st) return st;
+  if (!v_out) return fail(h, WAM_E_ARG, "null v_out");
+  if ((st = check_rr(h, rr))) return st;
+  return forward(h, k, x, cond, v_out, nullptr, rr, info);
+}
+
+int wam_denoise_step(wam_t h, int k, float* x, const float* cond, const wam_rr_profile* rr, wam_step_info* info) {
+  int st = check_step(h, k, x, cond);
+  if (st) return st;
+  if ((st = check_rr(h, rr))) return st;
+  return forward(h, k, x, cond, nullptr, x, rr, info);
+}
+
+int wam_continue(wam_t h, int k_from, int k_to, float* x, const float* cond, const wam_rr_profile* rr,
+                 int capture_stage, float* x_capture, wam_step_info* infos) {
+  if (!h) return WAM_E_ARG;
+  if (h->K <= 0) return fail(h, WAM_E_STATE, "schedule not set (wam_set_schedule)");
+  if (k_from < 0 || k_to > h->K || k_from > k_to) return fail(h, WAM_E_ARG, "need 0 <= k_from <= k_to <= K");
+  if (!x || !cond) return fail(h, WAM_E_ARG, "null trajectory or condition pointer");
+  int st = check_rr(h, rr);
+  if (st) return st;
+  return continue_impl(h, k_from, k_to, x, cond, rr, capture_stage, x_capture, infos);
+}
+
+int wam_hidden(wam_t h, int k, const float* x, const float* cond, int n_layers, float* h_out) {
+  int st = check_step(h, k, x, cond);
+  if (st) return st;
+  if (!h_out || n_layers < 0 || n_layers > h->d.L) return fail(h, WAM_E_ARG, "need 0 <= n_layers <= L");
+  if ((st = compute_conditioning(h, h->sigmas[k]))) return st;
+  if ((st = embed(h, x, cond))) return st;
+  if ((st = run_layers(h, 0, n_layers))) return st;
+  HIPCHK(h, hipMemcpyAsync(h_out, h->S(h->ws.h), (size_t)h->d.M * h->d.D * 4, hipMemcpyDeviceToDevice, h->stream));
+  return WAM_OK;
+}
+
+int wam_adapt_state(wam_t h, int op, const void* args) {
+  if (!h) return WAM_E_ARG;
+  const Dims& d = h->d;
+  switch (op) {
+    case WAM_ADAPT_REMAP: {
+      const wam_remap_args* a = static_cast<const wam_remap_args*>(args);
+      if (!a || !a->x_bar || !a->x_r || !a->noise || !a->x_out) return fail(h, WAM_E_ARG, "null remap argument");
+      if (!(a->sigma_r > 0.f)) return fail(h, WAM_E_ARG, "sigma_r must be > 0");
+      if (!(a->sigma_b0 >= 0.f)) return fail(h, WAM_E_ARG, "sigma_b0 must be >= 0");
+      if (a->shift_action < 0 || a->shift_video < 0) return fail(h, WAM_E_ARG, "shifts must be >= 0");
+      if (a->x_out == a->x_bar || a->x_out == a->x_r) return fail(h, WAM_E_ARG, "x_out must not alias inputs");
+      RemapArgs r{a->x_bar, a->x_r, a->noise, a->x_out, h->S<double>(h->ws.tr_rms), a->sigma_r, a->sigma_b0,
+                  a->shift_action, a->shift_video, d.B, d.Nv, d.Cv, d.Na, d.A};
+      HIPCHK(h, launch_remap(r, h->stream));
+      return WAM_OK;
+    }
+    case WAM_ADAPT_RESET_LAYER:
+      h->layer_valid = false;
+      return WAM_OK;
+    case WAM_ADAPT_RESET_ALL:
+      h->layer_valid = false;
+      h->has_prev = false;
+      h->kappa = 0;
+      return WAM_OK;
+    case WAM_ADAPT_SET_REPLAN: {
+      const wam_replan_state_args* a = static_cast<const wam_replan_state_args*>(args);
+      if (!a || !a->x_bar || !a->x_r || a->kappa < 0) return fail(h, WAM_E_ARG, "bad replan state");
+      int st = copy_traj(h, h->S(h->ws.x_bar), a->x_bar);
+      if (!st) st = copy_traj(h, h->S(h->ws.x_r), a->x_r);
+      if (st) return st;
+      h->kappa = a->kappa;
+      h->has_prev = true;
+      return WAM_OK;
+    }
+    default:
+      return fail(h, WAM_E_ARG, "unknown adapt op");
+  }
+}
+
+int wam_consistency_score(wam_t h, int n, const float* const* u_hat, const float* const* u, const int64_t* cnt,
+                          const double* delta, const double* weight, double* S_out) {
+  if (!h) return WAM_E_ARG;
+  if (n < 1 || n > WAM_MAX_COMPONENTS || !u_hat || !u || !cnt || !delta || !weight || !S_out)
+    return fail(h, WAM_E_ARG, "bad consistency-score arguments");
+  double wsum = 0.0;
+  for (int m = 0; m < n; ++m) {
+    if (!u_hat[m] || !u[m] || cnt[m] < 1 || !(delta[m] > 0.0) || !(weight[m] >= 0.0))
+      return fail(h, WAM_E_ARG, "component needs data, n >= 1, delta > 0, weight >= 0");
+    wsum += weight[m];
+  }
+  if (!(wsum > 0.0)) return fail(h, WAM_E_ARG, "weights sum to zero");
+  double* sums = h->S<double>(h->ws.or_sums);
+  HIPCHK(h, launch_or_sums(n, u_hat, u, cnt, delta, sums, h->stream));
+  HIPCHK(h, hipMemcpyAsync(h->host_stage, sums, n * 8, hipMemcpyDeviceToHost, h->stream));
+  HIPCHK(h, hipStreamSynchronize(h->stream));
+  double acc = 0.0;
+  for (int m = 0; m < n; ++m) {
+    const double e2 = h->host_stage[m] / (double)cnt[m];  // e_m^2
+    acc += weight[m] * e2;
+  }
+  *S_out = sqrt(acc / wsum);
+  return WAM_OK;
+}
+
+int wam_replan(wam_t h, const wam_replan_args* a, wam_replan_info* info) {
+  if (!h) return WAM_E_ARG;
+  if (!a || !a->cond_real || !a->x_out || !a->noise_remap) return fail(h, WAM_E_ARG, "null replan argument");
+  if (h->K <= 0) return fail(h, WAM_E_STATE, "schedule not set (wam_set_schedule)");
+  const int K = h->K;
+  if (a->b0 < 0 || a->b0 >= K) return fail(h, WAM_E_ARG, "need 0 <= b0 < K");
+  if (a->tr_enabled && !(a->b0 <= a->r && a->r < K)) return fail(h, WAM_E_ARG, "need b0 <= r < K");
+  if (!a->tr_enabled && !(0 <= a->r && a->r < K)) return fail(h, WAM_E_ARG, "need 0 <= r < K");
+  const int entry = a->tr_enabled ? a->b0 : 0;
+  if (a->or_enabled) {
+    if (!(0 < a->k1 && a->k1 < K - entry)) return fail(h, WAM_E_ARG, "need 0 < k1 < K - b0");
+    if (!a->cond_pred) return fail(h, WAM_E_ARG, "rebinding needs cond_pred");
+    if (a->kappa_max < 0) return fail(h, WAM_E_ARG, "kappa_max must be >= 0");
+  }
+  const bool rr_on = a->rr.mode != WAM_RR_OFF;
+  if (rr_on) {
+    int st = check_rr(h, &a->rr);
+    if (st) return st;
+  }
+  if (!h->has_prev && !a->noise_first) return fail(h, WAM_E_ARG, "first replan needs noise_first");
+
+  wam_replan_info loc{};
+  wam_replan_info* inf = info ? info : &loc;
+  memset(inf, 0, sizeof(*inf));
+  inf->S = -1.0;
+  for (int i = 0; i < WAM_MAX_STEPS; ++i) inf->decision[i] = -1;
+  const Dims& d = h->d;
+  float* x_bar = h->S(h->ws.x_bar);
+  float* x_r = h->S(h->ws.x_r);
+  float* x_init = h->S(h->ws.x_init);
+  float* xw = h->S(h->ws.x_work);
+  wam_step_info steps[WAM_MAX_STEPS * 2];
+  int nsteps = 0;
+  auto run = [&](int k0, int k1, const float* cond, bool rr_allowed) -> int {
+    const wam_rr_profile* rr = (rr_allowed && rr_on) ? &a->rr : nullptr;
+    int st = continue_impl(h, k0, k1, xw, cond, rr, a->r, x_r, steps + nsteps);
+    nsteps += k1 - k0;
+    return st;
+  };
+  int st;
+  h->layer_valid = false;  // layer state is scoped to one replan
+  if (!h->has_prev) {
+    if ((st = copy_traj(h, xw, a->noise_first))) return st;
+    if ((st = run(0, K, a->cond_real, a->rr_first))) return st;
+    inf->path = WAM_PATH_FIRST;
+  } else {
+    if (a->tr_enabled) {
+      RemapArgs r{x_bar, x_r, a->noise_remap, x_init, h->S<double>(h->ws.tr_rms), h->sigmas[a->r],
+                  h->sigmas[a->b0], a->shift_action, a->shift_video, d.B, d.Nv, d.Cv, d.Na, d.A};
+      HIPCHK(h, launch_remap(r, h->stream));
+    } else {
+      if ((st = copy_traj(h, x_init, a->noise_remap))) return st;
+    }
+    if ((st = copy_traj(h, xw, x_init))) return st;
+    if (a->or_enabled && h->kappa < a->kappa_max) {
+      inf->n_start = 1;
+      if ((st = run(entry, entry + a->k1, a->cond_pred, a->rr_prefix))) return st;
+      double S = 0.0;
+      st = wam_consistency_score(h, a->n_components, a->u_hat, a->u, a->n, a->delta, a->weight, &S);
+      if (st) return st;
+      inf->S = S;
+      if (S < a->tau && h->kappa < a->kappa_max) {
+        h->kappa += 1;
+        inf->n_bind = 1;
+        inf->path = WAM_PATH_ACCEPT;
+        if ((st = run(entry + a->k1, K, a->cond_real, a->rr_prefix))) return st;
+      } else {
+        h->kappa = 0;
+        inf->path = WAM_PATH_REJECT;
+        h->layer_valid = false;
+        if ((st = copy_traj(h, xw, x_init))) return st;
+        if ((st = run(entry, K, a->cond_real, a->rr_refresh))) return st;
+      }
+    } else {
+      inf->path = a->or_enabled ? WAM_PATH_FORCED : WAM_PATH_DIRECT;
+      if (a->or_enabled) h->kappa = 0;
+      if ((st = run(entry, K, a->cond_real, a->rr_refresh))) return st;
+    }
+  }
+  if ((st = copy_traj(h, x_bar, xw))) return st;
+  if ((st = copy_traj(h, a->x_out, xw))) return st;
+  h->has_prev = true;
+  inf->kappa = h->kappa;
+  inf->steps = nsteps;
+  for (int i = 0; i < nsteps; ++i) {
+    const wam_step_info& s = steps[i];
+    if (i < WAM_MAX_STEPS) inf->decision[i] = s.rr_attempted ? (int8_t)s.rr_accepted : (int8_t)-1;
+    inf->rr_attempts += s.rr_attempted;
+    inf->rr_reuses += s.rr_accepted;
+    inf->layers_skipped += s.layers_skipped;
+    if (s.rr_active) inf->layers_dense += d.L;
+  }
+  return WAM_OK;
+}
+
+int wam_get_replan_state(wam_t h, float* xb, float* xr, int32_t* kappa) {
+  if (!h) return WAM_E_ARG;
+  if (!h->has_prev) return fail(h, WAM_E_STATE, "no replan state yet");
+  int st;
+  if (xb && (st = copy_traj(h, xb, h->S(h->ws.x_bar)))) return st;
+  if (xr && (st = copy_traj(h, xr, h->S(h->ws.x_r)))) return st;
+  if (kappa) *kappa = h->kappa;
+  return WAM_OK;
+}
+
+int wam_profile_enable(wam_t h, int kc, int enable, int max_launches) {
+  if (!h) return WAM_E_ARG;
+  if (kc < 0 || kc >= WAM_KC_COUNT) return fail(h, WAM_E_ARG, "unknown kernel class");
+  ProfSlot& p = h->prof[kc];
+  if (!enable) {
+    p.on = false;
+    return WAM_OK;
+  }
+  if (max_launches < 1) return fail(h, WAM_E_ARG, "max_launches must be >= 1");
+  HIPCHK(h, hipStreamSynchronize(h->stream));
+  for (auto ev : p.ev) hipEventDestroy(ev);
+  p.ev.assign(2 * (size_t)max_launches, nullptr);
+  for (auto& ev : p.ev) HIPCHK(h, hipEventCreate(&ev));
+  p.work.assign(max_launches, 0.0);
+  p.max = max_launches;
+  p.used = 0;
+  p.on = true;
+  return WAM_OK;
+}
+
+int wam_profile_read(wam_t h, int kc, double* total_ms, int64_t* launches, double* work) {
+  if (!h) return WAM_E_ARG;
+  if (kc < 0 || kc >= WAM_KC_COUNT) return fail(h, WAM_E_ARG, "unknown kernel class");
+  HIPCHK(h, hipStreamSynchronize(h->stream));
+  ProfSlot& p = h->prof[kc];
+  double t = 0.0, w = 0.0;
+  for (int i = 0; i < p.used; ++i) {
+    float ms = 0.f;
+    HIPCHK(h, hipEventElapsedTime(&ms, p.ev[2 * i], p.ev[2 * i + 1]));
+    t += ms;
+    w += p.work[i];
+  }
+  if (total_ms) *total_ms = t;
+  if (launches) *launches = p.used;
+  if (work) *work = w;
+  return WAM_OK;
+}
+
+}  // extern "C"

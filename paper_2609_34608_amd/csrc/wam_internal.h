@@ -1,0 +1,163 @@
+// Internal declarations shared by the libwam translation units (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "wam.h"
+
+namespace wam {
+
+using bf16 = __bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------- helpers
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16 x) { return static_cast<float>(x); }
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return static_cast<bf16>(x); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// GELU, tanh form: x/2 (1 + tanh(sqrt(2/pi)(x + 0.044715 x^3))), with
+// tanh(u) = 1 - 2/(exp(2u)+1) written out so that large |u| saturates.
+__device__ __forceinline__ float gelu_tanh_f(float x) {
+  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
+  float u = k0 * (x + 0.044715f * x * x * x);
+  float t = 1.0f - 2.0f / (__expf(2.0f * u) + 1.0f);
+  return 0.5f * x * (1.0f + t);
+}
+
+// ---------------------------------------------------------------- GEMM
+enum GemmEpilogue : int {
+  EPI_BIAS = 0,       // out[m,n] = acc + bias[n]                       (act type)
+  EPI_BIAS_GELU = 1,  // out[m,n] = gelu(acc + bias[n])                 (act type)
+  EPI_GATED_RES = 2,  // h[m,n] += gate[n] * (acc + bias[n])            (float32)
+};
+
+struct GemmArgs {
+  const void* A;     // [M][K] activations (act type), row stride K
+  const void* W;     // [N][K] packed weight (act type), row stride K
+  const float* bias; // [N]
+  const float* gate; // [N] (EPI_GATED_RES)
+  void* out;         // [M][N] act type, or float h for EPI_GATED_RES
+  int M, N, K;
+  int epi;
+};
+
+hipError_t launch_gemm(const GemmArgs& a, bool bf16_mode, hipStream_t s);
+
+// ---------------------------------------------------------------- attention
+struct AttnArgs {
+  const void* q;   // [B*H][Tpad][dh]
+  const void* k;   // [B*H][Tpad][dh]
+  const void* vt;  // [B*H][dh][Tpad]
+  void* out;       // [B*T][D], head h at columns h*dh
+  int B, H, T, Tpad, dh, D;
+};
+hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s);
+
+// qkv [B*T][3D] -> q, k (optionally RMS-normalised with gains) and v^T
+struct RelayoutArgs {
+  const void* qkv;
+  const float* q_g;
+  const float* k_g;
+  void* q;
+  void* k;
+  void* vt;
+  int B, H, T, Tpad, dh, D;
+  int qk_norm;
+  float eps;
+};
+hipError_t launch_qkv_relayout(const RelayoutArgs& a, bool bf16_mode, hipStream_t s);
+
+// ---------------------------------------------------------------- small kernels
+// y[n] = out_act(sum_k in_act(x[k]) W[k][n] + b[n]), W row-major [K][N]
+// (float or bf16); act: 0 none, 1 SiLU.  partial: float[ceil(K/kc)][N].
+hipError_t launch_gemv(const float* x, const void* W, bool w_bf16, const float* b, float* y,
+                       float* partial, int K, int N, int in_act, int out_act, hipStream_t s);
+hipError_t launch_timestep_features(float sigma, float* e, int dim, hipStream_t s);
+
+struct EmbedArgs {
+  const float* x;     // [B][traj]
+  const float* cond;  // [B][No][Co]
+  const float* wv; const float* bv;  // [Cv][D], [D]
+  const float* wa; const float* ba;  // [A][D], [D]
+  const float* wo; const float* bo;  // [Co][D], [D]
+  float* h;           // [B][T][D]
+  int B, T, D, Nv, Cv, Na, A, No, Co;
+};
+hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
+
+// u = LN(h) * (1 + scale) + shift  (row-wise over D), u in act type
+hipError_t launch_ln_modulate(const float* h, const float* shift, const float* scale, void* u,
+                              int rows, int D, float eps, bool bf16_out, hipStream_t s);
+
+struct FinalArgs {
+  const float* h;      // [B][T][D]
+  const float* shift;  // [D]
+  const float* scale;  // [D]
+  const float* wv; const float* bv;  // [D][Cv], [Cv]
+  const float* wa; const float* ba;  // [D][A], [A]
+  float* v_out;        // [B][traj] or null
+  float* x;            // [B][traj] Euler target or null
+  float dsigma;        // sigma_{k+1} - sigma_k
+  int B, T, D, Nv, Cv, Na, A;
+  float eps;
+};
+hipError_t launch_final(const FinalArgs& a, hipStream_t s);
+
+// Residual Rescaling
+struct RRGateArgs {
+  const float* hs;   // h_s [M][D]
+  const float* hq;   // h_q
+  const float* pa;   // retained p_a
+  double* row_sums;  // [M][3]: sum p_i p_a, sum p_i^2, sum p_a^2
+  double* result;    // [B][2][8]: Sip Sii Saa alpha cos fit pass pad
+  int B, T, D, Nv, Na;
+  float alpha_min, alpha_max, eps, gamma_cos, gamma_fit;
+};
+hipError_t launch_rr_gate(const RRGateArgs& a, hipStream_t s);
+hipError_t launch_rr_inject(float* h, const float* Ra, const double* result, int B, int T, int D,
+                            int Nv, int Na, hipStream_t s);
+// p_a <- h - hq ; hq <- h   (before recomputing the middle)
+hipError_t launch_rr_pre_middle(const float* h, float* hq, float* pa, int64_t n, hipStream_t s);
+// R_a <- h - hq  (hq holds h_s)
+hipError_t launch_rr_refresh(const float* h, const float* hq, float* Ra, int64_t n, hipStream_t s);
+
+// Trajectory Remapping
+struct RemapArgs {
+  const float* x_bar; const float* x_r; const float* noise; float* x_out;
+  double* rms;  // [B][2] scratch
+  float sigma_r, sigma_b0;
+  int shift_action, shift_video;
+  int B, Nv, Cv, Na, A;
+};
+hipError_t launch_remap(const RemapArgs& a, hipStream_t s);
+
+// Observation Rebinding: sums of ((u_hat-u)/delta)^2 per component, float64
+hipError_t launch_or_sums(int n_comp, const float* const* u_hat, const float* const* u,
+                          const int64_t* n, const double* delta, double* sums, hipStream_t s);
+
+hipError_t launch_axpy_copy(const float* src, float* dst, int64_t n, hipStream_t s);
+
+}  // namespace wam

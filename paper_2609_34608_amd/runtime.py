@@ -1,0 +1,241 @@
+"""Python binding of libwam with the same entry points as the C ABI.
+
+PyTorch only provides device memory and the HIP stream; every step of the
+denoising path and of the adaptation operators runs in libwam's kernels.
+"""
+from __future__ import annotations
+
+import ctypes as C
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+from . import _lib as abi
+
+
+class WamError(RuntimeError):
+    pass
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, torch.Tensor):
+        if not t.is_cuda:
+            raise WamError("libwam takes device tensors only")
+        if t.dtype != torch.float32 or not t.is_contiguous():
+            raise WamError("device tensors must be contiguous float32")
+        return C.c_void_p(t.data_ptr())
+    return C.c_void_p(int(t))
+
+
+def host_weight_order(n_layers: int) -> list[str]:
+    """Names of the canonical host weight buffer, in the order wam.h documents."""
+    names = ["t_w1", "t_b1", "t_w2", "t_b2", "in_wv", "in_bv", "in_wa", "in_ba", "in_wo", "in_bo"]
+    for l in range(n_layers):
+        names += [f"l{l}.{n}" for n in ("mod_w", "mod_b", "qkv_w", "qkv_b", "q_g", "k_g", "proj_w",
+                                        "proj_b", "fc1_w", "fc1_b", "fc2_w", "fc2_b")]
+    names += ["f_mod_w", "f_mod_b", "out_wv", "out_bv", "out_wa", "out_ba"]
+    return names
+
+
+def make_config(B, L, D, H, F, Nv, Cv, Na, A, No, Co, dtype="bf16", qk_norm=True, ln_eps=1e-6) -> abi.WamConfig:
+    return abi.WamConfig(B=B, L=L, D=D, H=H, F=F, Nv=Nv, Cv=Cv, Na=Na, A=A, No=No, Co=Co,
+                       dtype=abi.WAM_BF16 if dtype == "bf16" else abi.WAM_FP32, qk_norm=int(bool(qk_norm)),
+                       ln_eps=ln_eps)
+
+
+def config_of(spec) -> abi.WamConfig:
+    """Config from any object exposing the model fields (B, L, D, ...)."""
+    return make_config(spec.B, spec.L, spec.D, spec.H, spec.F, spec.Nv, spec.Cv, spec.Na, spec.A,
+                       spec.No, spec.Co, spec.dtype, spec.qk_norm, spec.ln_eps)
+
+
+def rr_profile(q=0, s=0, e=0, mode=abi.WAM_RR_OFF, alpha_min=1.0, alpha_max=1.25, eps=1e-8,
+               gamma_cos=0.80, gamma_fit=0.60) -> abi.WamRRProfile:
+    return abi.WamRRProfile(q=q, s=s, e=e, mode=mode, alpha_min=alpha_min, alpha_max=alpha_max, eps=eps,
+                          gamma_cos=gamma_cos, gamma_fit=gamma_fit)
+
+
+@dataclass
+class StepInfo:
+    rr_active: bool
+    attempted: bool
+    accepted: bool
+    layers_evaluated: int
+    layers_skipped: int
+    alpha: np.ndarray
+    cos: np.ndarray
+    fit: np.ndarray
+
+    @classmethod
+    def of(cls, s: abi.WamStepInfo, B: int) -> "StepInfo":
+        a = np.array([[s.alpha[b][i] for i in range(2)] for b in range(B)])
+        c = np.array([[s.cos[b][i] for i in range(2)] for b in range(B)])
+        f = np.array([[s.fit[b][i] for i in range(2)] for b in range(B)])
+        return cls(bool(s.rr_active), bool(s.rr_attempted), bool(s.rr_accepted), s.layers_evaluated,
+                   s.layers_skipped, a, c, f)
+
+
+class WamModel:
+    """One libwam handle with its device weights and workspace (torch-owned)."""
+
+    def __init__(self, cfg: abi.WamConfig, weights: dict, device="cuda", stream: torch.cuda.Stream | None = None):
+        if not torch.cuda.is_available():
+            raise WamError("libwam needs a HIP device")
+        self.lib = abi.lib()
+        self.cfg = cfg
+        self.device = torch.device(device)
+        self.B = cfg.B
+        self.traj = int(self.lib.wam_traj_elems(C.byref(cfg)))
+        n_host = int(self.lib.wam_host_weight_count(C.byref(cfg)))
+        wbytes = int(self.lib.wam_weight_bytes(C.byref(cfg)))
+        wsbytes = int(self.lib.wam_workspace_bytes(C.byref(cfg)))
+        if n_host == 0 or wbytes == 0:
+            raise WamError("invalid configuration")
+        host = np.concatenate([np.ascontiguousarray(weights[n], np.float32).ravel()
+                               for n in host_weight_order(cfg.L)])
+        if host.size != n_host:
+            raise WamError(f"weight count {host.size} != {n_host}")
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        self.wdev = torch.empty(wbytes, dtype=torch.uint8, device=self.device)
+        self.ws = torch.empty(wsbytes, dtype=torch.uint8, device=self.device)
+        h = C.c_void_p()
+        st = self.lib.wam_init(C.byref(cfg), host.ctypes.data_as(C.c_void_p), host.size,
+                               C.c_void_p(self.wdev.data_ptr()), wbytes, C.c_void_p(self.ws.data_ptr()),
+                               wsbytes, C.c_void_p(self.stream.cuda_stream), C.byref(h))
+        if st != abi.WAM_OK:
+            raise WamError(f"wam_init failed: {self.lib.wam_status_string(st).decode()}")
+        self.h = h
+        self.K = 0
+
+    # ------------------------------------------------------------ helpers
+    def _check(self, st, what):
+        if st != abi.WAM_OK:
+            msg = self.lib.wam_last_error(self.h).decode()
+            raise WamError(f"{what}: {self.lib.wam_status_string(st).decode()}: {msg}")
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.lib.wam_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def new_traj(self):
+        return torch.empty((self.B, self.traj), dtype=torch.float32, device=self.device)
+
+    # ------------------------------------------------------------ ABI
+    def set_schedule(self, sigmas):
+        s = np.ascontiguousarray(sigmas, np.float32)
+        self._check(self.lib.wam_set_schedule(self.h, s.ctypes.data_as(C.POINTER(C.c_float)), s.size - 1),
+                    "wam_set_schedule")
+        self.K = s.size - 1
+
+    def velocity(self, k, x, cond, v_out=None, rr=None):
+        v_out = self.new_traj() if v_out is None else v_out
+        info = abi.WamStepInfo()
+        self._check(self.lib.wam_velocity(self.h, k, _ptr(x), _ptr(cond), _ptr(v_out),
+                                          C.byref(rr) if rr is not None else None, C.byref(info)),
+                    "wam_velocity")
+        return v_out, StepInfo.of(info, self.B)
+
+    def denoise_step(self, k, x, cond, rr=None):
+        info = abi.WamStepInfo()
+        self._check(self.lib.wam_denoise_step(self.h, k, _ptr(x), _ptr(cond),
+                                              C.byref(rr) if rr is not None else None, C.byref(info)),
+                    "wam_denoise_step")
+        return StepInfo.of(info, self.B)
+
+    def continue_(self, k_from, k_to, x, cond, rr=None, capture_stage=-1, x_capture=None):
+        n = max(k_to - k_from, 1)
+        infos = (abi.WamStepInfo * n)()
+        self._check(self.lib.wam_continue(self.h, k_from, k_to, _ptr(x), _ptr(cond),
+                                          C.byref(rr) if rr is not None else None, capture_stage,
+                                          _ptr(x_capture), infos), "wam_continue")
+        return [StepInfo.of(infos[i], self.B) for i in range(k_to - k_from)]
+
+    def hidden(self, k, x, cond, n_layers, h_out=None):
+        if h_out is None:
+            T = self.cfg.Nv + self.cfg.Na + self.cfg.No
+            h_out = torch.empty((self.B, T, self.cfg.D), dtype=torch.float32, device=self.device)
+        self._check(self.lib.wam_hidden(self.h, k, _ptr(x), _ptr(cond), n_layers, _ptr(h_out)), "wam_hidden")
+        return h_out
+
+    def remap(self, x_bar, x_r, sigma_r, sigma_b0, shift_action, shift_video, noise, x_out=None):
+        x_out = self.new_traj() if x_out is None else x_out
+        a = abi.WamRemapArgs(x_bar=_ptr(x_bar), x_r=_ptr(x_r), sigma_r=sigma_r, sigma_b0=sigma_b0,
+                           shift_action=shift_action, shift_video=shift_video, noise=_ptr(noise), x_out=_ptr(x_out))
+        self._check(self.lib.wam_adapt_state(self.h, abi.WAM_ADAPT_REMAP, C.byref(a)), "wam_adapt_state(REMAP)")
+        return x_out
+
+    def reset_layer_state(self):
+        self._check(self.lib.wam_adapt_state(self.h, abi.WAM_ADAPT_RESET_LAYER, None), "RESET_LAYER")
+
+    def reset_all(self):
+        self._check(self.lib.wam_adapt_state(self.h, abi.WAM_ADAPT_RESET_ALL, None), "RESET_ALL")
+
+    def set_replan_state(self, x_bar, x_r, kappa):
+        a = abi.WamReplanStateArgs(x_bar=_ptr(x_bar), x_r=_ptr(x_r), kappa=kappa)
+        self._check(self.lib.wam_adapt_state(self.h, abi.WAM_ADAPT_SET_REPLAN, C.byref(a)), "SET_REPLAN")
+
+    def get_replan_state(self):
+        xb, xr = self.new_traj(), self.new_traj()
+        kappa = C.c_int32()
+        self._check(self.lib.wam_get_replan_state(self.h, _ptr(xb), _ptr(xr), C.byref(kappa)),
+                    "wam_get_replan_state")
+        return xb, xr, kappa.value
+
+    def consistency_score(self, u_hat, u, delta, weight):
+        n = len(u_hat)
+        uh = (C.c_void_p * n)(*[_ptr(t).value for t in u_hat])
+        uu = (C.c_void_p * n)(*[_ptr(t).value for t in u])
+        cnt = (C.c_int64 * n)(*[t.numel() for t in u])
+        dl = (C.c_double * n)(*delta)
+        wt = (C.c_double * n)(*weight)
+        S = C.c_double()
+        self._check(self.lib.wam_consistency_score(self.h, n, uh, uu, cnt, dl, wt, C.byref(S)),
+                    "wam_consistency_score")
+        return S.value
+
+    def replan(self, cond_real, x_out, noise_remap, *, cond_pred=None, u_hat=(), u=(), delta=(), weight=(),
+               noise_first=None, rr=None, b0=0, r=0, shift_action=0, shift_video=0, k1=0, tau=0.5,
+               kappa_max=3, tr_enabled=True, or_enabled=True, rr_first=True, rr_prefix=True,
+               rr_refresh=True):
+        a = abi.WamReplanArgs()
+        a.cond_real = _ptr(cond_real)
+        a.cond_pred = _ptr(cond_pred)
+        a.n_components = len(u)
+        for m in range(len(u)):
+            a.u_hat[m] = _ptr(u_hat[m]).value
+            a.u[m] = _ptr(u[m]).value
+            a.n[m] = u[m].numel()
+            a.delta[m] = delta[m]
+            a.weight[m] = weight[m]
+        a.noise_first = _ptr(noise_first)
+        a.noise_remap = _ptr(noise_remap)
+        a.x_out = _ptr(x_out)
+        a.rr = rr if rr is not None else rr_profile()
+        a.b0, a.r, a.shift_action, a.shift_video, a.k1 = b0, r, shift_action, shift_video, k1
+        a.tau, a.kappa_max = tau, kappa_max
+        a.tr_enabled, a.or_enabled = int(tr_enabled), int(or_enabled)
+        a.rr_first, a.rr_prefix, a.rr_refresh = int(rr_first), int(rr_prefix), int(rr_refresh)
+        info = abi.WamReplanInfo()
+        self._check(self.lib.wam_replan(self.h, C.byref(a), C.byref(info)), "wam_replan")
+        return info
+
+    def sync(self):
+        self._check(self.lib.wam_sync(self.h), "wam_sync")
+
+    def profile_enable(self, kc, enable=True, max_launches=4096):
+        self._check(self.lib.wam_profile_enable(self.h, kc, int(enable), max_launches), "wam_profile_enable")
+
+    def profile_read(self, kc):
+        t, n, w = C.c_double(), C.c_int64(), C.c_double()
+        self._check(self.lib.wam_profile_read(self.h, kc, C.byref(t), C.byref(n), C.byref(w)), "wam_profile_read")
+        return t.value, n.value, w.value

@@ -1,0 +1,58 @@
+"""Helpers shared by the GPU parity tests (device plumbing only)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import method as OM
+from synth import get_workload, make_weights
+
+
+def device():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    return torch.device("cuda:0")
+
+
+def to_dev(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+
+
+def rel_err(got, ref):
+    """max_i |got_i - ref_i| / max_i |ref_i| (the parity measure)."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    return float(np.max(np.abs(got - ref)) / np.max(np.abs(ref)))
+
+
+def rr_of(spec, mode, **kw):
+    """(GPU profile, oracle profile) pair with the workload's RR constants."""
+    from paper_2609_34608_amd import runtime as R
+    q, s, e = spec.rr_bounds
+    p = dict(alpha_min=spec.rr_alpha_min, alpha_max=spec.rr_alpha_max, eps=spec.rr_eps,
+             gamma_cos=spec.rr_gamma_cos, gamma_fit=spec.rr_gamma_fit)
+    p.update(kw)
+    # the device compares in float32 thresholds; give the oracle the same values
+    po = {k: float(np.float32(v)) for k, v in p.items()}
+    return R.rr_profile(q, s, e, mode, **p), OM.RRProfile(q, s, e, mode=mode, **po)
+
+
+def f32_sigmas(K, shift=1.0):
+    """Schedule as the device sees it (float32), widened for the oracle."""
+    return OM.flow_schedule(K, shift).astype(np.float32).astype(np.float64)
+
+
+_MODELS = {}
+
+
+def model_for(name, dev, **wkw):
+    """Cached (spec, weights, WamModel) per workload and weight options."""
+    from paper_2609_34608_amd import runtime as R
+    key = (name, tuple(sorted(wkw.items())))
+    if key not in _MODELS:
+        spec = get_workload(name)
+        if "B" in wkw:
+            spec = spec.replace(B=wkw["B"])
+        W = make_weights(spec, **{k: v for k, v in wkw.items() if k != "B"})
+        m = R.WamModel(R.config_of(spec), W, device=dev)
+        _MODELS[key] = (spec, W, m)
+    return _MODELS[key]

@@ -1,0 +1,253 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle.
+
+Tolerances (max |got - ref| / max |ref| per compared tensor): 1e-4 in fp32
+mode; 2e-2 on the final action chunk in bf16 mode.  Residual-Rescaling
+decisions follow the decision-trace protocol: the oracle is forced to the
+device's accept/refresh trace and the per-step statistics are compared.
+"""
+from collections import deque
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import dit as OD, method as OM
+from synth import get_workload, make_weights, make_initial_noise, make_observations, make_remap_noise
+from gpu_common import device, to_dev, rel_err, rr_of, f32_sigmas, model_for
+
+pytestmark = pytest.mark.gpu
+
+FP32_TOL = 1e-4
+BF16_TOL = 2e-2
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return device()
+
+
+def _tiny(dev, name="tiny", B=1):
+    spec, W, m = model_for(name, dev, B=B, bias_std=0.02, gain_std=0.1)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    return spec, W, m, sig
+
+
+# ------------------------------------------------------------------ fp32, layer level
+def test_tiny_hidden_states_per_layer(dev):
+    spec, W, m, sig = _tiny(dev, B=2)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    for k in (0, 2):
+        for n in range(spec.L + 1):
+            got = m.hidden(k, to_dev(x0, dev), to_dev(cond, dev), n).cpu().numpy()
+            ref = OD.hidden_after(W, spec, x0, cond, sig[k], n)
+            err = rel_err(got, ref)
+            assert err <= 1e-5, (k, n, err)
+
+
+def test_tiny_velocity_each_step(dev):
+    spec, W, m, sig = _tiny(dev)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    for k in range(spec.K):
+        v, _ = m.velocity(k, to_dev(x0, dev), to_dev(cond, dev))
+        ref = OD.velocity(W, spec, x0, cond, sig[k])
+        assert rel_err(v.cpu().numpy(), ref) <= FP32_TOL, k
+
+
+def test_tiny_native_chunk_and_capture(dev):
+    spec, W, m, sig = _tiny(dev)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    x = to_dev(x0, dev)
+    cap = torch.zeros_like(x)
+    m.continue_(0, spec.K, x, to_dev(cond, dev), capture_stage=2, x_capture=cap)
+    ref, ref_cap, _ = OM.denoise(W, spec, x0, cond, sig, 0, spec.K, None, OM.LayerState(), capture_stage=2)
+    assert rel_err(x.cpu().numpy(), ref) <= FP32_TOL
+    assert rel_err(cap.cpu().numpy(), ref_cap) <= FP32_TOL
+    # the action chunk specifically
+    a_got = OM.action_chunk(spec, x.cpu().numpy())
+    assert rel_err(a_got, OM.action_chunk(spec, ref)) <= FP32_TOL
+
+
+def test_determinism(dev):
+    spec, W, m, sig = _tiny(dev)
+    x0 = to_dev(make_initial_noise(spec), dev)
+    c = to_dev(make_observations(spec, 0)[0], dev)
+    outs = []
+    for _ in range(2):
+        x = x0.clone()
+        m.continue_(0, spec.K, x, c)
+        outs.append(x.cpu().numpy())
+    np.testing.assert_array_equal(outs[0], outs[1])
+
+
+# ------------------------------------------------------------------ Residual Rescaling
+@pytest.mark.parametrize("mode_name", ["AUTO", "FORCE_SKIP", "FORCE_FULL", "NEVER"])
+def test_rr_modes_match_oracle(dev, mode_name):
+    from paper_2609_34608_amd import _lib as L
+    spec, W, m, sig = _tiny(dev, "tiny_rr", B=2)
+    modes = {"AUTO": (L.WAM_RR_AUTO, {}), "FORCE_SKIP": (L.WAM_RR_FORCE_SKIP, {}),
+             "FORCE_FULL": (L.WAM_RR_FORCE_FULL, {}), "NEVER": (L.WAM_RR_AUTO, {"gamma_cos": 1.5})}
+    mode, kw = modes[mode_name]
+    rr_g, rr_o = rr_of(spec, mode, **kw)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    m.reset_layer_state()
+    x = to_dev(x0, dev)
+    infos = m.continue_(0, spec.K, x, to_dev(cond, dev), rr=rr_g)
+    trace = deque(i.accepted for i in infos if i.attempted)
+    st = OM.LayerState()
+    ref, _, oinfos = OM.denoise(W, spec, x0, cond, sig, 0, spec.K, rr_o, st, forced=trace)
+    assert rel_err(x.cpu().numpy(), ref) <= FP32_TOL
+    for gi, oi in zip(infos, oinfos):
+        assert gi.attempted == oi.attempted and gi.accepted == oi.accepted
+        assert gi.layers_evaluated == oi.layers_evaluated
+        if gi.attempted:
+            np.testing.assert_allclose(gi.alpha, oi.alpha, atol=1e-4)
+            np.testing.assert_allclose(gi.cos, oi.cos, atol=1e-4)
+            np.testing.assert_allclose(gi.fit, oi.fit, atol=1e-3)
+    if mode_name in ("FORCE_FULL", "NEVER"):
+        assert not any(i.accepted for i in infos)
+    if mode_name == "FORCE_SKIP":
+        assert all(i.accepted for i in infos[1:])
+
+
+def test_rr_identity_adaptation(dev):
+    """The same step twice: the second reuses with alpha = 1, cos = 1, fit ~ 0."""
+    from paper_2609_34608_amd import _lib as L
+    spec, W, m, sig = _tiny(dev, "tiny_rr", B=2)
+    rr_g, _ = rr_of(spec, L.WAM_RR_AUTO)
+    x0 = to_dev(make_initial_noise(spec), dev)
+    c = to_dev(make_observations(spec, 0)[0], dev)
+    m.reset_layer_state()
+    v1, i1 = m.velocity(1, x0, c, rr=rr_g)
+    v1 = v1.clone()
+    v2, i2 = m.velocity(1, x0, c, rr=rr_g)
+    assert not i1.attempted and i2.attempted and i2.accepted
+    np.testing.assert_allclose(i2.alpha, 1.0, atol=1e-6)
+    np.testing.assert_allclose(i2.cos, 1.0, atol=1e-6)
+    assert np.all(i2.fit < 1e-3)
+    assert rel_err(v2.cpu().numpy(), v1.cpu().numpy()) <= 1e-5
+
+
+# ------------------------------------------------------------------ TR and OR
+@pytest.mark.parametrize("shift_a,shift_v", [(0, 0), (3, 0), (5, 7), (16, 0), (20, 64)])
+def test_remap_matches_oracle(dev, shift_a, shift_v):
+    spec, W, m, sig = _tiny(dev, B=2)
+    rng = np.random.default_rng(11)
+    xb, xr, eps = (rng.standard_normal((spec.B, spec.traj)).astype(np.float32) for _ in range(3))
+    sr, sb = np.float32(0.6), np.float32(0.75)
+    got = m.remap(to_dev(xb, dev), to_dev(xr, dev), float(sr), float(sb), shift_a, shift_v, to_dev(eps, dev))
+    d = OM.tr_direction(spec, xr, xb, float(sr))
+    ref = OM.tr_remap(spec, xb, d, float(sb), shift_a, shift_v, eps)
+    assert rel_err(got.cpu().numpy(), ref) <= 1e-6
+
+
+def test_consistency_score_matches_oracle(dev):
+    spec, W, m, sig = _tiny(dev)
+    rng = np.random.default_rng(12)
+    comps = [(rng.standard_normal(n).astype(np.float32), rng.standard_normal(n).astype(np.float32))
+             for n in (100, 7, 4096)]
+    delta, weight = [255.0, 2.0, 0.5], [0.5, 0.3, 0.2]
+    S = m.consistency_score([to_dev(a, dev) for a, _ in comps], [to_dev(b, dev) for _, b in comps], delta, weight)
+    errs = [OM.or_component_error(a, b, dl) for (a, b), dl in zip(comps, delta)]
+    assert S == pytest.approx(OM.or_score(errs, weight), rel=1e-12)
+
+
+# ------------------------------------------------------------------ joint runtime
+def _replan_args(spec):
+    q = spec
+    return dict(b0=q.tr_b0, r=q.tr_r, shift_action=q.shift_action, shift_video=q.shift_video, k1=q.or_k1,
+                tau=q.or_tau, kappa_max=q.or_kappa_max)
+
+
+@pytest.mark.parametrize("tau", [0.5, 0.3])
+def test_closed_loop_replans_match_oracle(dev, tau):
+    """Teacher-forced per replan: the oracle starts from the device's retained
+    state and follows its RR decision trace."""
+    from paper_2609_34608_amd import _lib as L
+    spec, W, m, sig = _tiny(dev, "tiny_replay")
+    spec = spec.replace(or_tau=tau)
+    rr_g, rr_o = rr_of(spec, L.WAM_RR_AUTO)
+    ra = _replan_args(spec)
+    rho = spec.ar_rho
+    delta = 1.0 / np.sqrt(1 - rho * rho)
+    obs = make_observations(spec, spec.control_steps)
+    m.reset_all()
+    prof = OM.RuntimeProfile(**ra)
+    rt = OM.ReplanRuntime(W, spec, sig, rr_o, prof)
+    x_out = m.new_traj()
+    paths = []
+    for t in range(spec.control_steps):
+        c_real = obs[t]
+        c_pred = (rho * obs[t - 1]).astype(np.float32) if t > 0 else obs[t]
+        if t > 0:
+            xb, xr, kappa = m.get_replan_state()
+            rt.set_state(xb.cpu().numpy(), xr.cpu().numpy(), kappa)
+        cr, cp = to_dev(c_real, dev), to_dev(c_pred, dev)
+        info = m.replan(cr, x_out, to_dev(make_remap_noise(spec, t), dev), cond_pred=cp, u_hat=[cp], u=[cr],
+                        delta=[delta], weight=[1.0], noise_first=to_dev(make_initial_noise(spec), dev),
+                        rr=rr_g, **ra)
+        trace = deque(int(d) for d in info.decision[:info.steps] if d >= 0)
+        ref, rinfo = rt.replan(c_real, c_pred, [c_pred], [c_real], [delta], [1.0],
+                               noise_first=make_initial_noise(spec), noise_remap=make_remap_noise(spec, t),
+                               forced=trace)
+        assert info.path == rinfo.path, t
+        assert info.steps == rinfo.steps and info.kappa == rinfo.kappa
+        if rinfo.S is not None:
+            assert info.S == pytest.approx(rinfo.S, rel=1e-9)
+        assert rel_err(x_out.cpu().numpy(), ref) <= FP32_TOL, t
+        paths.append(info.path)
+    if tau == 0.5:  # S ~ 0.44 < 0.5: accepted until kappa reaches kappa_max
+        assert paths == [L.WAM_PATH_FIRST, L.WAM_PATH_ACCEPT, L.WAM_PATH_ACCEPT, L.WAM_PATH_ACCEPT,
+                         L.WAM_PATH_FORCED, L.WAM_PATH_ACCEPT][:len(paths)]
+    else:
+        assert all(p == L.WAM_PATH_REJECT for p in paths[1:])
+
+
+# ------------------------------------------------------------------ bf16 workloads
+def test_small_bf16_native_chunk(dev):
+    spec, W, m = model_for("small", dev)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    v, _ = m.velocity(0, to_dev(x0, dev), to_dev(cond, dev))
+    vref = OD.velocity(W, spec, x0, cond, sig[0])
+    ev = rel_err(v.cpu().numpy(), vref)
+    print(f"small bf16 velocity(step 0) rel err {ev:.3e}")
+    assert ev <= BF16_TOL
+    x = to_dev(x0, dev)
+    m.continue_(0, spec.K, x, to_dev(cond, dev))
+    ref, _, _ = OM.denoise(W, spec, x0, cond, sig, 0, spec.K, None, OM.LayerState())
+    ea = rel_err(OM.action_chunk(spec, x.cpu().numpy()), OM.action_chunk(spec, ref))
+    print(f"small bf16 action chunk rel err {ea:.3e}")
+    assert ea <= BF16_TOL
+
+
+@pytest.mark.parametrize("name,layers", [("mid", (0, 11)), ("large", (0, 17))])
+def test_full_size_layer_sampled_rows(dev, name, layers):
+    """One DiT layer at full size (bf16 GEMMs and attention at their real
+    shapes), checked on sampled rows that the oracle computes one by one."""
+    spec, W, m = model_for(name, dev)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    k = 3
+    c = OD.cond_vector(W, sig[k])
+    rng = np.random.default_rng(5)
+    rows = np.unique(np.r_[0, spec.M - 1, spec.T - 1, spec.Nv, spec.Nv + spec.Na,
+                           rng.integers(0, spec.M, 12)])
+    for l in layers:
+        h_in = m.hidden(k, to_dev(x0, dev), to_dev(cond, dev), l).cpu().numpy()
+        h_out = m.hidden(k, to_dev(x0, dev), to_dev(cond, dev), l + 1).cpu().numpy().reshape(-1, spec.D)
+        ref = OD.dit_layer_rows(W, spec, l, h_in, c, rows)
+        # compare the layer's update, which is what the bf16 contractions produce
+        upd_got = h_out[rows] - h_in.reshape(-1, spec.D)[rows]
+        upd_ref = ref - h_in.reshape(-1, spec.D)[rows]
+        e = rel_err(upd_got, upd_ref)
+        print(f"{name} layer {l} sampled-row update rel err {e:.3e}")
+        assert e <= BF16_TOL, (l, e)
