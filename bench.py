@@ -35,6 +35,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-native", action="store_true")
     p.add_argument("--cpu-sample-steps", type=int, default=5)
+    p.add_argument("--rr-mode", default="auto", choices=["auto", "force_skip", "force_full", "off"],
+                   help="residual-rescaling mode of the timed replans")
     return p.parse_args()
 
 
@@ -60,7 +62,9 @@ def main():
     sig = (1.0 - s / K)  # uniform flow schedule sigma_k = 1 - k/K
     m.set_schedule(sig)
     q, s_, e = spec.rr_bounds
-    rr = R.rr_profile(q, s_, e, L.WAM_RR_AUTO, spec.rr_alpha_min, spec.rr_alpha_max, spec.rr_eps,
+    modes = {"auto": L.WAM_RR_AUTO, "force_skip": L.WAM_RR_FORCE_SKIP, "force_full": L.WAM_RR_FORCE_FULL,
+             "off": L.WAM_RR_OFF}
+    rr = R.rr_profile(q, s_, e, modes[args.rr_mode], spec.rr_alpha_min, spec.rr_alpha_max, spec.rr_eps,
                       spec.rr_gamma_cos, spec.rr_gamma_fit)
     n_ctrl = 1 + args.warmup + args.steps
     obs = make_observations(spec, n_ctrl)
@@ -74,7 +78,7 @@ def main():
     ra = dict(b0=spec.tr_b0, r=spec.tr_r, shift_action=spec.shift_action, shift_video=spec.shift_video,
               k1=spec.or_k1, tau=spec.or_tau, kappa_max=spec.or_kappa_max)
 
-    def replan(t):
+    def replan(t, rr=rr):
         cr = obs_d[t]
         cp = pred_d[t - 1] if t > 0 else obs_d[t]
         return m.replan(cr, x_out, remap_noise[t], cond_pred=cp, u_hat=[cp], u=[cr], delta=[delta],
@@ -169,6 +173,26 @@ def main():
             "class_ms_one_replan": {L.KERNEL_CLASS_NAMES[k]: round(v, 4) for k, v in tot.items()},
         },
     }
+
+    # adaptation kernels at this workload's size: two extra (untimed) replans
+    # with reuse forced so that the gate, the injection and the refresh all run
+    rr_force = R.rr_profile(q, s_, e, L.WAM_RR_FORCE_SKIP, spec.rr_alpha_min, spec.rr_alpha_max, spec.rr_eps,
+                            spec.rr_gamma_cos, spec.rr_gamma_fit)
+    ad = [L.WAM_KC_RR_GATE, L.WAM_KC_RR_INJECT, L.WAM_KC_RR_REFRESH]
+    for kc in ad:
+        m.profile_enable(kc, True, 4096)
+    for _ in range(2):
+        replan(t - 1, rr=rr_force)
+    adapt = {}
+    for kc in ad:
+        ms_, n_, bytes_ = m.profile_read(kc)
+        m.profile_enable(kc, False)
+        if n_:
+            gbs = bytes_ / (ms_ * 1e-3) / 1e9
+            adapt[L.KERNEL_CLASS_NAMES[kc]] = {"launches": n_, "avg_us": round(1000.0 * ms_ / n_, 3),
+                                               "bytes_per_launch": bytes_ / n_, "GB/s": round(gbs, 1),
+                                               "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
+    out["adaptation_kernels"] = adapt
 
     if not args.no_native:
         # full re-denoise of the same model: K native steps from noise per chunk

@@ -100,8 +100,9 @@ extern "C" {
 
 typedef struct wam_handle *wam_t;
 
-/* Model configuration.  D % H == 0, head size D/H in {32, 64};
- * bf16 mode additionally needs D/H == 64, D % 128 == 0, F % 128 == 0. */
+/* Model configuration.  D % 64 == 0 (D <= 2048), D % H == 0, head size D/H in
+ * {32, 64}, Cv <= 16, A <= 16, Co <= 64; bf16 mode additionally needs
+ * D/H == 64, D % 128 == 0 and F % 128 == 0. */
 typedef struct {
   int32_t B;       /* batch (samples denoised together), 1..WAM_MAX_BATCH */
   int32_t L;       /* DiT layers                                            */

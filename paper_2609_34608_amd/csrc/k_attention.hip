@@ -72,7 +72,7 @@ constexpr int kKB = 64;           // keys per tile
 constexpr int kKL = kDh + 8;      // LDS row (K tile): 64 dh + pad
 constexpr int kVL = kKB + 8;      // LDS row (V^T tile): 64 keys + pad
 
-template <int QT, int NW>
+template <int QT, int NW, int PF>
 __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float scale_log2) {
   constexpr int NT = NW * 64;
   constexpr int QB = NW * QT * 16;  // queries per block
@@ -112,35 +112,31 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
     lrun[qt] = 0.f;
   }
 
-  // tile loads: 64x64 bf16 = 512 chunks of 16 B for K and for V^T
+  // K and V^T tiles of 64 keys: 512 chunks of 16 B each, CH per thread;
+  // register slots hold the next PF tiles (slot of tile t is t % PF)
   constexpr int CH = 512 / NT;
-  uint4 rk[CH], rv[CH];
-  auto gload = [&](int k0) {
+  static_assert(CH >= 1 && CH * NT == 512, "tile load split");
+  u32x4 rk[PF][CH], rv[PF][CH];
+  auto gload = [&](auto S, int k0) __attribute__((always_inline)) {
+    constexpr int slot = decltype(S)::value;
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
-      rk[i] = *reinterpret_cast<const uint4*>(Kg + (size_t)(k0 + row) * kDh + col);
-      rv[i] = *reinterpret_cast<const uint4*>(Vg + (size_t)row * a.Tpad + k0 + col);
+      rk[slot][i] = *reinterpret_cast<const u32x4*>(Kg + (size_t)(k0 + row) * kDh + col);
+      rv[slot][i] = *reinterpret_cast<const u32x4*>(Vg + (size_t)row * a.Tpad + k0 + col);
     }
   };
-  auto sstore = [&](int buf) {
+  auto sstore = [&](auto S, int buf) __attribute__((always_inline)) {
+    constexpr int slot = decltype(S)::value;
 #pragma unroll
     for (int i = 0; i < CH; ++i) {
       const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
-      *reinterpret_cast<uint4*>(&Ks[buf][row][col]) = rk[i];
-      *reinterpret_cast<uint4*>(&Vs[buf][row][col]) = rv[i];
+      *reinterpret_cast<u32x4*>(&Ks[buf][row][col]) = rk[slot][i];
+      *reinterpret_cast<u32x4*>(&Vs[buf][row][col]) = rv[slot][i];
     }
   };
 
-  const int nkb = a.Tpad / kKB;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kb = 0; kb < nkb; ++kb) {
-    const int buf = kb & 1;
-    const int k0 = kb * kKB;
-    if (kb + 1 < nkb) gload(k0 + kKB);
-
+  auto block = [&](int buf, int k0) __attribute__((always_inline)) {
     // S^T tiles [key tile kt][query tile qt]
     f32x4 s[4][QT];
 #pragma unroll
@@ -176,7 +172,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
       const float mnew = fmaxf(mrun[qt], mx * scale_log2);
-      const float corr = exp2f(mrun[qt] - mnew);
+      const float corr = __builtin_amdgcn_exp2f(mrun[qt] - mnew);
       mrun[qt] = mnew;
       float ls = 0.f;
       float p[4][4];
@@ -184,7 +180,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          p[kt][r] = exp2f(s[kt][qt][r] * scale_log2 - mnew);
+          p[kt][r] = __builtin_amdgcn_exp2f(s[kt][qt][r] * scale_log2 - mnew);
           ls += p[kt][r];
         }
       lrun[qt] = lrun[qt] * corr + ls;
@@ -217,8 +213,25 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
           o[d][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[c][qt], o[d][qt], 0, 0, 0);
       }
     }
-    if (kb + 1 < nkb) sstore(buf ^ 1);
-    __syncthreads();
+  };
+
+  const int nkb = a.Tpad / kKB;
+  static_for<PF>([&](auto P) __attribute__((always_inline)) {
+    if (decltype(P)::value < nkb) gload(P, decltype(P)::value * kKB);
+  });
+  sstore(std::integral_constant<int, 0>{}, 0);
+  __syncthreads();
+  for (int kb0 = 0; kb0 < nkb; kb0 += PF) {
+    static_for<PF>([&](auto J) __attribute__((always_inline)) {
+      constexpr int j = decltype(J)::value;
+      const int kb = kb0 + j;
+      if (kb < nkb) {
+        if (kb + PF < nkb) gload(J, (kb + PF) * kKB);  // slot j held tile kb, already in LDS
+        block(kb & 1, kb * kKB);
+        if (kb + 1 < nkb) sstore(std::integral_constant<int, (j + 1) % PF>{}, (kb + 1) & 1);
+        __syncthreads();
+      }
+    });
   }
 
   // normalise and store O[b*T + q][h*64 + dh]; lane holds dh = d*16 + 4g + r of query lr
@@ -295,20 +308,27 @@ hipError_t launch_qkv_relayout(const RelayoutArgs& a, bool bf16_mode, hipStream_
   return hipGetLastError();
 }
 
+hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, hipStream_t s) {
+  if (a.dh != kDh || a.Tpad % kKB) return hipErrorInvalidValue;
+  const float scale_log2 = 1.4426950408889634f / sqrtf((float)a.dh);
+  const int qb = qt * nw * 16;
+  dim3 grid((a.T + qb - 1) / qb, a.B * a.H);
+  if (qt == 1 && nw == 2) attn_bf16_kernel<1, 2, 3><<<grid, 128, 0, s>>>(a, scale_log2);
+  else if (qt == 1 && nw == 4) attn_bf16_kernel<1, 4, 3><<<grid, 256, 0, s>>>(a, scale_log2);
+  else if (qt == 2 && nw == 4) attn_bf16_kernel<2, 4, 3><<<grid, 256, 0, s>>>(a, scale_log2);
+  else if (qt == 4 && nw == 4) attn_bf16_kernel<4, 4, 2><<<grid, 256, 0, s>>>(a, scale_log2);
+  else if (qt == 2 && nw == 8) attn_bf16_kernel<2, 8, 3><<<grid, 512, 0, s>>>(a, scale_log2);
+  else if (qt == 1 && nw == 8) attn_bf16_kernel<1, 8, 3><<<grid, 512, 0, s>>>(a, scale_log2);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s) {
   if (bf16_mode) {
-    if (a.dh != kDh || a.Tpad % kKB) return hipErrorInvalidValue;
-    const float scale_log2 = 1.4426950408889634f / sqrtf((float)a.dh);
-    // 32 queries per wave when that still gives >= 2 blocks per CU
-    const long blocks32 = (long)((a.T + 127) / 128) * a.B * a.H;
-    if (blocks32 >= 512) {
-      dim3 grid((a.T + 127) / 128, a.B * a.H);
-      attn_bf16_kernel<2, 4><<<grid, 256, 0, s>>>(a, scale_log2);
-    } else {
-      dim3 grid((a.T + 63) / 64, a.B * a.H);
-      attn_bf16_kernel<1, 4><<<grid, 256, 0, s>>>(a, scale_log2);
-    }
-    return hipGetLastError();
+    // 8 waves x 32 queries when that still fills the chip, else 4 waves x 16
+    const long blocks = (long)((a.T + 255) / 256) * a.B * a.H;
+    if (blocks >= 256) return launch_attention_cfg(a, 2, 8, s);
+    return launch_attention_cfg(a, 1, 4, s);
   }
   dim3 grid((a.T + 63) / 64, a.B * a.H);
   if (a.dh == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(a);

@@ -1,155 +1,73 @@
-// Projection GEMMs of the DiT block with fused epilogues (gfx950).
-//
-//   C[M][N] = A[M][K] . W[N][K]^T      (both operands K-contiguous)
-//
-// bf16 path: v_mfma_f32_16x16x32_bf16, 256 threads = 4 waves in a 2x2 grid,
-// block tile BM x BN x 64, LDS double buffer filled from a register prefetch
-// of the next K tile, padded LDS rows (64+8 bf16) so that the 16 lanes of an
-// MFMA operand read hit distinct banks.  Blocks are renumbered so that each
-// XCD (blocks are dispatched round-robin over the 8 XCDs) gets a contiguous
-// run of a grouped tile order and shares A rows / W columns in its own L2.
-//
-// fp32 path: plain LDS-tiled FMA kernel (used by the float32 parity mode).
-#include "wam_internal.h"
+// Projection GEMMs of the DiT block: tile-configuration table, planner and
+// dispatch for the bf16 MFMA kernel of gemm_tile.h, plus a plain LDS-tiled
+// fp32 kernel for the float32 parity mode.
+#include "gemm_tile.h"
 
 namespace wam {
 
 namespace {
 
-constexpr int kBK = 64;
-constexpr int kPad = 8;
-constexpr int kLds = kBK + kPad;  // bf16 elements per LDS row
-constexpr int kThreads = 256;
-constexpr int kGroupM = 8;
-constexpr int kXcd = 8;
+using gemm::launch_tile;
 
-__device__ __forceinline__ void tile_coords(int bid, int nblocks, int tiles_m, int tiles_n,
-                                            int& tm, int& tn) {
-  // XCD-contiguous renumbering (bijective for round-robin dispatch).
-  const int per = nblocks / kXcd, rem = nblocks % kXcd;
-  const int x = bid % kXcd, idx = bid / kXcd;
-  const int logical = x * per + min(x, rem) + idx;
-  // grouped order: kGroupM tile rows swept column by column
-  const int width = kGroupM * tiles_n;
-  const int group = logical / width;
-  const int first_m = group * kGroupM;
-  const int gsz = min(tiles_m - first_m, kGroupM);
-  const int in = logical % width;
-  tm = first_m + in % gsz;
-  tn = in / gsz;
+// ---------------------------------------------------------------- configs
+struct TileCfg {
+  int bm, bn, wgm, wgn, pf;
+};
+// index: tile rows x cols, waves (rows x cols), K tiles in flight
+constexpr TileCfg kCfgs[] = {
+    {64, 64, 2, 2, 4},    // 0
+    {64, 128, 2, 2, 4},   // 1
+    {128, 64, 2, 2, 4},   // 2
+    {128, 128, 2, 2, 3},  // 3
+    {128, 128, 2, 4, 4},  // 4
+    {256, 128, 4, 2, 3},  // 5
+    {128, 256, 2, 4, 3},  // 6
+    {256, 256, 4, 4, 2},  // 7
+    {256, 128, 2, 2, 2},  // 8
+    {128, 256, 2, 2, 2},  // 9
+};
+constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
+
+template <int C, int ROLE>
+hipError_t launch_c(const GemmArgs& a, int splits, hipStream_t s) {
+  constexpr TileCfg t = kCfgs[C];
+  return launch_tile<t.bm, t.bn, t.wgm, t.wgn, t.pf, ROLE>(a, splits, s);
 }
 
-template <int EPI, typename TOut>
-__device__ __forceinline__ void epilogue_store(const GemmArgs& a, int m, int n, float acc) {
+template <int ROLE>
+hipError_t launch_role(const GemmArgs& a, int cfg, int splits, hipStream_t s) {
+  switch (cfg) {
+    case 0: return launch_c<0, ROLE>(a, splits, s);
+    case 1: return launch_c<1, ROLE>(a, splits, s);
+    case 2: return launch_c<2, ROLE>(a, splits, s);
+    case 3: return launch_c<3, ROLE>(a, splits, s);
+    case 4: return launch_c<4, ROLE>(a, splits, s);
+    case 5: return launch_c<5, ROLE>(a, splits, s);
+    case 6: return launch_c<6, ROLE>(a, splits, s);
+    case 7: return launch_c<7, ROLE>(a, splits, s);
+    case 8: return launch_c<8, ROLE>(a, splits, s);
+    default: return launch_c<9, ROLE>(a, splits, s);
+  }
+}
+
+bool qkv_ok(int c) { return (kCfgs[c].bn / kCfgs[c].wgn) % 64 == 0; }
+
+// ---------------------------------------------------------------- fp32
+constexpr int kFT = 64, kFK = 16;
+
+template <int EPI>
+__device__ __forceinline__ void epi1_f32(const GemmArgs& a, int m, int n, float acc) {
   if (m >= a.M) return;
   const float v = acc + a.bias[n];
   if constexpr (EPI == EPI_GATED_RES) {
     float* h = static_cast<float*>(a.out) + (size_t)m * a.N + n;
     *h += a.gate[n] * v;
   } else if constexpr (EPI == EPI_BIAS_GELU) {
-    static_cast<TOut*>(a.out)[(size_t)m * a.N + n] = from_f32<TOut>(gelu_tanh_f(v));
+    static_cast<float*>(a.out)[(size_t)m * a.N + n] = gelu_tanh_f(v);
   } else {
-    static_cast<TOut*>(a.out)[(size_t)m * a.N + n] = from_f32<TOut>(v);
+    static_cast<float*>(a.out)[(size_t)m * a.N + n] = v;
   }
 }
-
-template <int BM, int BN, int EPI>
-__global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(GemmArgs a) {
-  constexpr int WM = BM / 2, WN = BN / 2;  // wave tile
-  constexpr int TM = WM / 16, TN = WN / 16;
-  constexpr int ACH = BM * (kBK / 8) / kThreads;  // 16-byte chunks per thread
-  constexpr int BCH = BN * (kBK / 8) / kThreads;
-  static_assert(ACH >= 1 && BCH >= 1, "tile too small");
-
-  __shared__ __attribute__((aligned(16))) bf16 As[2][BM][kLds];
-  __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN][kLds];
-
-  const int tiles_m = (a.M + BM - 1) / BM, tiles_n = a.N / BN;
-  int tm, tn;
-  tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
-  const int m0 = tm * BM, n0 = tn * BN;
-  const int tid = threadIdx.x, lane = tid % kWave, wid = tid / kWave;
-  const int wm = wid / 2, wn = wid % 2;
-  const bf16* A = static_cast<const bf16*>(a.A);
-  const bf16* W = static_cast<const bf16*>(a.W);
-  const int K = a.K;
-
-  uint4 ra[ACH], rb[BCH];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int c = tid + kThreads * i, row = c >> 3, col = (c & 7) * 8;
-      const int m = m0 + row;
-      ra[i] = m < a.M ? *reinterpret_cast<const uint4*>(A + (size_t)m * K + k0 + col)
-                      : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      const int c = tid + kThreads * i, row = c >> 3, col = (c & 7) * 8;
-      rb[i] = *reinterpret_cast<const uint4*>(W + (size_t)(n0 + row) * K + k0 + col);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int c = tid + kThreads * i, row = c >> 3, col = (c & 7) * 8;
-      *reinterpret_cast<uint4*>(&As[buf][row][col]) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      const int c = tid + kThreads * i, row = c >> 3, col = (c & 7) * 8;
-      *reinterpret_cast<uint4*>(&Bs[buf][row][col]) = rb[i];
-    }
-  };
-
-  f32x4 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const int nk = K / kBK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  const int lr = lane % 16, lk = (lane / 16) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * kBK);
-#pragma unroll
-    for (int ks = 0; ks < kBK / 32; ++ks) {
-      bf16x8 af[TM], bfr[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(&As[buf][wm * WM + i * 16 + lr][ks * 32 + lk]);
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8*>(&Bs[buf][wn * WN + j * 16 + lr][ks * 32 + lk]);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < nk) sstore(buf ^ 1);
-    __syncthreads();
-  }
-
-  // accumulator (i,j) element r: row i*16 + 4*(lane/16) + r, column j*16 + lane%16
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = m0 + wm * WM + i * 16 + (lane / 16) * 4 + r;
-        const int n = n0 + wn * WN + j * 16 + lr;
-        epilogue_store<EPI, bf16>(a, m, n, acc[i][j][r]);
-      }
-}
-
-// ---------------------------------------------------------------- fp32
-constexpr int kFT = 64, kFK = 16;
 
 template <int EPI>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
@@ -192,33 +110,61 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int n = n0 + tx * 4 + j;
-      if (n < a.N) epilogue_store<EPI, float>(a, m0 + ty * 4 + i, n, acc[i][j]);
+      if (n < a.N) epi1_f32<EPI>(a, m0 + ty * 4 + i, n, acc[i][j]);
     }
-}
-
-template <int BM, int BN>
-hipError_t launch_bf16_tile(const GemmArgs& a, hipStream_t s) {
-  const int blocks = ((a.M + BM - 1) / BM) * (a.N / BN);
-  switch (a.epi) {
-    case EPI_BIAS: gemm_bf16_kernel<BM, BN, EPI_BIAS><<<blocks, kThreads, 0, s>>>(a); break;
-    case EPI_BIAS_GELU: gemm_bf16_kernel<BM, BN, EPI_BIAS_GELU><<<blocks, kThreads, 0, s>>>(a); break;
-    case EPI_GATED_RES: gemm_bf16_kernel<BM, BN, EPI_GATED_RES><<<blocks, kThreads, 0, s>>>(a); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
 }
 
 }  // namespace
 
+int gemm_num_configs() { return kNumCfgs; }
+
+GemmPlan plan_gemm(int M, int N, int K, int epi) {
+  // Chosen from a sweep of every tile configuration at the workload shapes:
+  // the 256x256 tile with 16 waves wins whenever M gives ~8+ tile rows; below
+  // that, 64x64 tiles (64x128 for the QKV epilogue, which needs whole heads
+  // per wave), with K split into >= 768-deep slices while that adds blocks.
+  GemmPlan p{0, 1};
+  if (M >= 2048 && N % 256 == 0) {
+    p.cfg = 7;
+    return p;
+  }
+  if (epi == EPI_QKV) {
+    p.cfg = N % 128 == 0 ? 1 : 3;
+    return p;
+  }
+  const long blocks = (long)((M + 63) / 64) * (N / 64);
+  while (blocks * p.splits < 384 && K / (p.splits * 2) >= 768 && K % (gemm::kBK * p.splits * 2) == 0 &&
+         p.splits < 8)
+    p.splits *= 2;
+  return p;
+}
+
+size_t gemm_partial_floats(int M, int N, int K, int epi) {
+  const GemmPlan p = plan_gemm(M, N, K, epi);
+  return p.splits > 1 ? (size_t)p.splits * M * N : 0;
+}
+
+hipError_t launch_gemm_cfg(const GemmArgs& a, int cfg, int splits, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  if (cfg < 0 || cfg >= kNumCfgs || splits < 1) return hipErrorInvalidValue;
+  if (a.K % (gemm::kBK * splits) || a.N % kCfgs[cfg].bn || a.N % 4) return hipErrorInvalidValue;
+  if (splits > 1 && (a.epi == EPI_QKV || !a.partial)) return hipErrorInvalidValue;
+  if (a.epi == EPI_QKV && !qkv_ok(cfg)) return hipErrorInvalidValue;
+  switch (a.role) {
+    case 0: return launch_role<0>(a, cfg, splits, s);
+    case 1: return launch_role<1>(a, cfg, splits, s);
+    case 2: return launch_role<2>(a, cfg, splits, s);
+    default: return launch_role<3>(a, cfg, splits, s);
+  }
+}
+
 hipError_t launch_gemm(const GemmArgs& a, bool bf16_mode, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   if (bf16_mode) {
-    if (a.K % kBK || a.N % 64) return hipErrorInvalidValue;
-    const long big = (long)((a.M + 127) / 128) * (a.N / 128);
-    if (a.N % 128 == 0 && big >= 2L * 256) return launch_bf16_tile<128, 128>(a, s);
-    return launch_bf16_tile<64, 64>(a, s);
+    const GemmPlan p = plan_gemm(a.M, a.N, a.K, a.epi);
+    return launch_gemm_cfg(a, p.cfg, p.splits, s);
   }
-  if (a.K % kFK) return hipErrorInvalidValue;
+  if (a.K % kFK || a.epi == EPI_QKV) return hipErrorInvalidValue;
   dim3 grid((a.N + kFT - 1) / kFT, (a.M + kFT - 1) / kFT);
   switch (a.epi) {
     case EPI_BIAS: gemm_f32_kernel<EPI_BIAS><<<grid, 256, 0, s>>>(a); break;

@@ -22,16 +22,46 @@ __device__ __forceinline__ double block_sum_d(double v, double* sh) {
   return t;
 }
 
-// ------------------------------------------------------------- timestep
-// e = [cos(t f_i), sin(t f_i)], t = 1000 sigma, f_i = 10000^(-i/half)
-__global__ void timestep_features_kernel(float sigma, float* e, int dim) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  const int half = dim / 2;
-  if (i >= dim) return;
-  const int j = i < half ? i : i - half;
-  const double t = 1000.0 * (double)sigma;
-  const double f = exp(-log(10000.0) * (double)j / (double)half);
-  e[i] = (float)(i < half ? cos(t * f) : sin(t * f));
+// ------------------------------------------------------------- timestep MLP
+// Small GEMV for the conditioning MLP: block = 64 outputs x 16 K-groups,
+// y[n] = SiLU(sum_k x[k] W[k][n] + b[n]).  With FEATURES the input is
+// computed in-kernel from sigma: x = [cos(t f_i), sin(t f_i)], t = 1000 sigma,
+// f_i = 10000^(-i/128) (float64 arguments).
+constexpr int kTimeDim = 256;
+constexpr int kSgN = 64, kSgK = 16;
+template <bool FEATURES>
+__global__ __launch_bounds__(kSgN* kSgK) void small_gemv_silu_kernel(float sigma, const float* __restrict__ x,
+                                                                    const float* __restrict__ W,
+                                                                    const float* __restrict__ b,
+                                                                    float* __restrict__ y, int K, int N) {
+  __shared__ float xs[2048];
+  __shared__ float part[kSgK][kSgN + 1];
+  const int tid = threadIdx.x, nl = tid % kSgN, kg = tid / kSgN;
+  for (int k = tid; k < K; k += blockDim.x) {
+    if constexpr (FEATURES) {
+      const int half = K / 2;
+      const int j = k < half ? k : k - half;
+      const double t = 1000.0 * (double)sigma;
+      const double f = exp(-log(10000.0) * (double)j / (double)half);
+      xs[k] = (float)(k < half ? cos(t * f) : sin(t * f));
+    } else {
+      xs[k] = x[k];
+    }
+  }
+  __syncthreads();
+  const int n = blockIdx.x * kSgN + nl;
+  float acc = 0.f;
+  if (n < N) {
+#pragma unroll 4
+    for (int k = kg; k < K; k += kSgK) acc += xs[k] * W[(size_t)k * N + n];
+  }
+  part[kg][nl] = acc;
+  __syncthreads();
+  if (kg == 0 && n < N) {
+    float s = b[n];
+    for (int g = 0; g < kSgK; ++g) s += part[g][nl];
+    y[n] = s / (1.0f + __expf(-s));
+  }
 }
 
 // ------------------------------------------------------------- GEMV
@@ -149,61 +179,101 @@ __global__ void ln_modulate_kernel(const float* __restrict__ h, const float* __r
     }
 }
 
-// ------------------------------------------------------------- final layer + Euler
-// One wave per trajectory row (video or action token): LN + final
-// modulation, output head (W^T packed [Cout][D]), optional velocity store and
-// fused Euler update x += dsigma * v.
-__global__ void final_kernel(FinalArgs a, const float* __restrict__ wvT,
-                             const float* __restrict__ waT) {
-  const int nrow = a.Nv + a.Na;
-  const int gw = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+// Vectorised form for D % 256 == 0 and bf16 output: lane holds
+// elements 4 lane + 256 i .. +3 (16-byte loads, 8-byte stores).
+constexpr int kMaxV4 = 8;  // D <= 2048
+__global__ void ln_modulate_v4_kernel(const float* __restrict__ h, const float* __restrict__ shift,
+                                      const float* __restrict__ scale, bf16* __restrict__ u, int rows,
+                                      int D, float eps) {
+  const int row = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
-  if (gw >= a.B * nrow) return;
-  const int b = gw / nrow, t = gw % nrow;
-  const float* hr = a.h + ((size_t)b * a.T + t) * a.D;
-  const int vpl = a.D / kWave;
-  float v[kMaxVpl];
+  if (row >= rows) return;
+  const f32x4* hr = reinterpret_cast<const f32x4*>(h + (size_t)row * D);
+  const int n4 = D / 256;
+  f32x4 v[kMaxV4];
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < kMaxVpl; ++i)
-    if (i < vpl) {
+  for (int i = 0; i < kMaxV4; ++i)
+    if (i < n4) {
       v[i] = hr[lane + kWave * i];
-      s += v[i];
+      s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
     }
-  const float mean = wave_sum(s) / (float)a.D;
+  const float mean = wave_sum(s) / (float)D;
   float q = 0.f;
 #pragma unroll
-  for (int i = 0; i < kMaxVpl; ++i)
-    if (i < vpl) {
-      const float d = v[i] - mean;
-      q += d * d;
+  for (int i = 0; i < kMaxV4; ++i)
+    if (i < n4) {
+      const float a = v[i].x - mean, b = v[i].y - mean, c = v[i].z - mean, d = v[i].w - mean;
+      q += (a * a + b * b) + (c * c + d * d);
     }
-  const float rstd = rsqrtf(wave_sum(q) / (float)a.D + a.eps);
+  const float rstd = rsqrtf(wave_sum(q) / (float)D + eps);
 #pragma unroll
-  for (int i = 0; i < kMaxVpl; ++i)
-    if (i < vpl) {
-      const int c = lane + kWave * i;
-      v[i] = (v[i] - mean) * rstd * (1.0f + a.scale[c]) + a.shift[c];
+  for (int i = 0; i < kMaxV4; ++i)
+    if (i < n4) {
+      const int c = 4 * (lane + kWave * i);
+      const float4 sc = *reinterpret_cast<const float4*>(scale + c);
+      const float4 sh = *reinterpret_cast<const float4*>(shift + c);
+      bf16x4 o = {static_cast<bf16>((v[i].x - mean) * rstd * (1.0f + sc.x) + sh.x),
+                  static_cast<bf16>((v[i].y - mean) * rstd * (1.0f + sc.y) + sh.y),
+                  static_cast<bf16>((v[i].z - mean) * rstd * (1.0f + sc.z) + sh.z),
+                  static_cast<bf16>((v[i].w - mean) * rstd * (1.0f + sc.w) + sh.w)};
+      *reinterpret_cast<bf16x4*>(u + (size_t)row * D + c) = o;
     }
+}
+
+// ------------------------------------------------------------- final layer + Euler
+// Four trajectory rows per wave; lane = (row r = lane/16, output channel
+// o = lane%16).  The 16 lanes of a row compute its LayerNorm statistics
+// together, stage the modulated row in LDS, then each lane forms one output
+// v[r][o] = u[r] . W^T[o] + b[o] (W^T packed [Cout][D], read through L1/L2),
+// stores the velocity and/or applies the Euler update x += dsigma v.
+constexpr int kFinalWaves = 1;
+__global__ __launch_bounds__(kFinalWaves * 64) void final_kernel(FinalArgs a) {
+  extern __shared__ float us[];  // [kFinalWaves * 4][D]
+  const int nrow = a.Nv + a.Na;
+  const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
+  const int r = lane / 16, o = lane % 16;
+  const int grow = (blockIdx.x * kFinalWaves + wid) * 4 + r;  // global trajectory row
+  const bool valid = grow < a.B * nrow;
+  const int b = valid ? grow / nrow : 0, t = valid ? grow % nrow : 0;
+  float* ur = us + (size_t)(wid * 4 + r) * a.D;
+  const float* hr = a.h + ((size_t)b * a.T + t) * a.D;
+  // LayerNorm statistics over the 16 lanes of this row (xor < 16 stays in the row)
+  float s = 0.f;
+  for (int c = o; c < a.D; c += 16) s += valid ? hr[c] : 0.f;
+#pragma unroll
+  for (int m = 8; m > 0; m >>= 1) s += __shfl_xor(s, m, 64);
+  const float mean = s / (float)a.D;
+  float q = 0.f;
+  for (int c = o; c < a.D; c += 16) {
+    const float d = (valid ? hr[c] : 0.f) - mean;
+    q += d * d;
+  }
+#pragma unroll
+  for (int m = 8; m > 0; m >>= 1) q += __shfl_xor(q, m, 64);
+  const float rstd = rsqrtf(q / (float)a.D + a.eps);
+  for (int c = o; c < a.D; c += 16)
+    ur[c] = valid ? (hr[c] - mean) * rstd * (1.0f + a.scale[c]) + a.shift[c] : 0.f;
+  __syncthreads();
   const bool video = t < a.Nv;
   const int cout = video ? a.Cv : a.A;
-  const float* wT = video ? wvT : waT;
-  const float* bias = video ? a.bv : a.ba;
-  const int traj = a.Nv * a.Cv + a.Na * a.A;
-  const size_t base = (size_t)b * traj + (video ? (size_t)t * a.Cv
-                                                : (size_t)a.Nv * a.Cv + (size_t)(t - a.Nv) * a.A);
-  for (int o = 0; o < cout; ++o) {
-    float p = 0.f;
+  if (!valid || o >= cout) return;
+  const float* w = (video ? a.wv : a.wa) + (size_t)o * a.D;
+  // D % 64 == 0: 16 independent 16-byte weight loads in flight per step
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int c0 = 0; c0 < a.D; c0 += 64) {
+    f32x4 wv[16];
 #pragma unroll
-    for (int i = 0; i < kMaxVpl; ++i)
-      if (i < vpl) p += v[i] * wT[(size_t)o * a.D + lane + kWave * i];
-    p = wave_sum(p);
-    if (lane == 0) {
-      const float vel = p + bias[o];
-      if (a.v_out) a.v_out[base + o] = vel;
-      if (a.x) a.x[base + o] += a.dsigma * vel;
-    }
+    for (int i = 0; i < 16; ++i) wv[i] = *reinterpret_cast<const f32x4*>(w + c0 + 4 * i);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc += *reinterpret_cast<const f32x4*>(ur + c0 + 4 * i) * wv[i];
   }
+  const float vel = (acc[0] + acc[1]) + (acc[2] + acc[3]) + (video ? a.bv : a.ba)[o];
+  const int traj = a.Nv * a.Cv + a.Na * a.A;
+  const size_t idx = (size_t)b * traj + (video ? (size_t)t * a.Cv + o
+                                               : (size_t)a.Nv * a.Cv + (size_t)(t - a.Nv) * a.A + o);
+  if (a.v_out) a.v_out[idx] = vel;
+  if (a.x) a.x[idx] += a.dsigma * vel;
 }
 
 // ------------------------------------------------------------- Residual Rescaling
@@ -397,8 +467,12 @@ __global__ void or_sums_kernel(OrSumArgs a) {
 }  // namespace
 
 // ================================================================ launchers
-hipError_t launch_timestep_features(float sigma, float* e, int dim, hipStream_t s) {
-  timestep_features_kernel<<<(dim + 255) / 256, 256, 0, s>>>(sigma, e, dim);
+hipError_t launch_timestep_mlp(float sigma, const float* w1, const float* b1, const float* w2, const float* b2,
+                               float* a1, float* silu_c, int D, hipStream_t s) {
+  if (D > 2048) return hipErrorInvalidValue;
+  const int grid = (D + kSgN - 1) / kSgN;
+  small_gemv_silu_kernel<true><<<grid, kSgN * kSgK, 0, s>>>(sigma, nullptr, w1, b1, a1, kTimeDim, D);
+  small_gemv_silu_kernel<false><<<grid, kSgN * kSgK, 0, s>>>(0.f, a1, w2, b2, silu_c, D, D);
   return hipGetLastError();
 }
 
@@ -426,7 +500,9 @@ hipError_t launch_ln_modulate(const float* h, const float* shift, const float* s
   if (D % kWave || D / kWave > kMaxVpl) return hipErrorInvalidValue;
   const int wpb = 4;
   dim3 grid((rows + wpb - 1) / wpb);
-  if (bf16_out)
+  if (bf16_out && D % 256 == 0)
+    ln_modulate_v4_kernel<<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (bf16*)u, rows, D, eps);
+  else if (bf16_out)
     ln_modulate_kernel<bf16><<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (bf16*)u, rows, D, eps);
   else
     ln_modulate_kernel<float><<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (float*)u, rows, D, eps);
@@ -434,10 +510,11 @@ hipError_t launch_ln_modulate(const float* h, const float* shift, const float* s
 }
 
 hipError_t launch_final(const FinalArgs& a, hipStream_t s) {
-  if (a.D % kWave || a.D / kWave > kMaxVpl) return hipErrorInvalidValue;
-  const int wpb = 4;
+  if (a.D % 4 || a.Cv > 16 || a.A > 16) return hipErrorInvalidValue;
   const int rows = a.B * (a.Nv + a.Na);
-  final_kernel<<<(rows + wpb - 1) / wpb, wpb * kWave, 0, s>>>(a, a.wv, a.wa);
+  const int per_block = kFinalWaves * 4;
+  const size_t lds = (size_t)per_block * a.D * sizeof(float);
+  final_kernel<<<(rows + per_block - 1) / per_block, kFinalWaves * 64, lds, s>>>(a);
   return hipGetLastError();
 }
 

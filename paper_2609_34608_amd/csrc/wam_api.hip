@@ -47,7 +47,7 @@ int make_dims(const wam_config* c, Dims* d, std::string* why) {
   if (c->L < 1 || c->D < 64 || c->H < 1 || c->F < 64) return bad("L, D, H, F out of range");
   if (c->Nv < 0 || c->Na < 1 || c->No < 0 || c->Cv < 1 || c->A < 1 || c->Co < 1)
     return bad("token counts / channels out of range");
-  if (c->Cv > 64 || c->A > 64 || c->Co > 64) return bad("Cv, A, Co must be <= 64");
+  if (c->Cv > 16 || c->A > 16 || c->Co > 64) return bad("Cv and A must be <= 16, Co <= 64");
   if (c->D % c->H) return bad("D must be divisible by H");
   if (c->D % 64 || c->D > 2048) return bad("D must be a multiple of 64 and <= 2048");
   if (c->dtype != WAM_FP32 && c->dtype != WAM_BF16) return bad("dtype must be WAM_FP32 or WAM_BF16");
@@ -159,7 +159,7 @@ DevLayout dev_layout(const Dims& d) {
 
 struct WsLayout {
   size_t h, hq, pa, Ra, u, qkv, q, k, vt, attn, mlp, e, a1, sc, mod, gpart, v;
-  size_t x_bar, x_r, x_init, x_work, rr_rows, rr_res, tr_rms, or_sums, total;
+  size_t x_bar, x_r, x_init, x_work, rr_rows, rr_res, tr_rms, or_sums, gsplit, total;
   size_t gpart_floats;
 };
 
@@ -191,6 +191,14 @@ WsLayout ws_layout(const Dims& d) {
   w.rr_res = take((size_t)d.B * 2 * 8 * 8);
   w.tr_rms = take((size_t)d.B * 2 * 8);
   w.or_sums = take(WAM_MAX_COMPONENTS * 8);
+  size_t split = 0;
+  if (d.bf) {
+    split = std::max(split, gemm_partial_floats(d.M, 3 * d.D, d.D, EPI_QKV));
+    split = std::max(split, gemm_partial_floats(d.M, d.D, d.D, EPI_GATED_RES));
+    split = std::max(split, gemm_partial_floats(d.M, d.F, d.D, EPI_BIAS_GELU));
+    split = std::max(split, gemm_partial_floats(d.M, d.D, d.F, EPI_GATED_RES));
+  }
+  w.gsplit = take(std::max<size_t>(split, 1) * 4);
   w.total = o;
   return w;
 }
@@ -270,11 +278,8 @@ int compute_conditioning(wam_t h, float sigma) {
   const DevLayout& wl = h->wl;
   const WsLayout& ws = h->ws;
   hipStream_t s = h->stream;
-  HIPCHK(h, launch_timestep_features(sigma, h->S(ws.e), kTimeDim, s));
-  HIPCHK(h, launch_gemv(h->S(ws.e), h->W(wl.t_w1), false, h->W(wl.t_b1), h->S(ws.a1), h->S(ws.gpart),
-                        kTimeDim, d.D, 0, 1, s));
-  HIPCHK(h, launch_gemv(h->S(ws.a1), h->W(wl.t_w2), false, h->W(wl.t_b2), h->S(ws.sc), h->S(ws.gpart),
-                        d.D, d.D, 0, 1, s));
+  HIPCHK(h, launch_timestep_mlp(sigma, h->W(wl.t_w1), h->W(wl.t_b1), h->W(wl.t_w2), h->W(wl.t_b2), h->S(ws.a1),
+                                h->S(ws.sc), d.D, s));
   // sc now holds SiLU(c); all adaLN modulations in one pass
   HIPCHK(h, launch_gemv(h->S(ws.sc), h->W<char>(wl.wmod), d.bf, h->W(wl.bmod), h->S(ws.mod),
                         h->S(ws.gpart), d.D, d.Nmod, 0, 0, s));
@@ -320,13 +325,24 @@ int run_layer(wam_t h, int l) {
   HIPCHK(h, launch_ln_modulate(hh, mod + 0 * D, mod + 1 * D, h->S<char>(ws.u), d.M, d.D, h->cfg.ln_eps, d.bf, s));
   {
     ProfScope ps(h, WAM_KC_GEMM_QKV, 2.0 * M * D * 3 * D);
-    GemmArgs g{h->S<char>(ws.u), qkv_w, qkv_b, nullptr, h->S<char>(ws.qkv), d.M, (int)(3 * D), (int)D, EPI_BIAS};
-    HIPCHK(h, launch_gemm(g, d.bf, s));
+    GemmArgs g{};
+    g.A = h->S<char>(ws.u); g.W = qkv_w; g.bias = qkv_b; g.M = d.M; g.N = (int)(3 * D); g.K = (int)D;
+    g.role = 0; g.partial = h->S(ws.gsplit);
+    if (d.bf) {
+      // projection with q/k RMS-norm and the head-major relayout fused in
+      g.epi = EPI_QKV;
+      g.qkv = QkvOut{h->S<bf16>(ws.q), h->S<bf16>(ws.k), h->S<bf16>(ws.vt), q_g, k_g,
+                     d.T, d.Tpad, d.H, d.D, h->cfg.qk_norm, h->cfg.ln_eps};
+      HIPCHK(h, launch_gemm(g, true, s));
+    } else {
+      g.epi = EPI_BIAS; g.out = h->S<char>(ws.qkv);
+      HIPCHK(h, launch_gemm(g, false, s));
+    }
   }
-  {
+  if (!d.bf) {
     RelayoutArgs r{h->S<char>(ws.qkv), q_g, k_g, h->S<char>(ws.q), h->S<char>(ws.k), h->S<char>(ws.vt),
                    d.B, d.H, d.T, d.Tpad, d.dh, d.D, h->cfg.qk_norm, h->cfg.ln_eps};
-    HIPCHK(h, launch_qkv_relayout(r, d.bf, s));
+    HIPCHK(h, launch_qkv_relayout(r, false, s));
   }
   {
     ProfScope ps(h, WAM_KC_ATTENTION, 4.0 * d.B * (double)d.T * d.T * D);
@@ -336,18 +352,21 @@ int run_layer(wam_t h, int l) {
   }
   {
     ProfScope ps(h, WAM_KC_GEMM_PROJ, 2.0 * M * D * D);
-    GemmArgs g{h->S<char>(ws.attn), proj_w, proj_b, mod + 2 * D, hh, d.M, (int)D, (int)D, EPI_GATED_RES};
+    GemmArgs g{h->S<char>(ws.attn), proj_w, proj_b, mod + 2 * D, hh, d.M, (int)D, (int)D, EPI_GATED_RES, 1,
+               h->S(ws.gsplit), {}};
     HIPCHK(h, launch_gemm(g, d.bf, s));
   }
   HIPCHK(h, launch_ln_modulate(hh, mod + 3 * D, mod + 4 * D, h->S<char>(ws.u), d.M, d.D, h->cfg.ln_eps, d.bf, s));
   {
     ProfScope ps(h, WAM_KC_GEMM_FC1, 2.0 * M * D * d.F);
-    GemmArgs g{h->S<char>(ws.u), fc1_w, fc1_b, nullptr, h->S<char>(ws.mlp), d.M, d.F, (int)D, EPI_BIAS_GELU};
+    GemmArgs g{h->S<char>(ws.u), fc1_w, fc1_b, nullptr, h->S<char>(ws.mlp), d.M, d.F, (int)D, EPI_BIAS_GELU, 2,
+               h->S(ws.gsplit), {}};
     HIPCHK(h, launch_gemm(g, d.bf, s));
   }
   {
     ProfScope ps(h, WAM_KC_GEMM_FC2, 2.0 * M * D * d.F);
-    GemmArgs g{h->S<char>(ws.mlp), fc2_w, fc2_b, mod + 5 * D, hh, d.M, (int)D, d.F, EPI_GATED_RES};
+    GemmArgs g{h->S<char>(ws.mlp), fc2_w, fc2_b, mod + 5 * D, hh, d.M, (int)D, d.F, EPI_GATED_RES, 3,
+               h->S(ws.gsplit), {}};
     HIPCHK(h, launch_gemm(g, d.bf, s));
   }
   return WAM_OK;

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 #include "wam.h"
 
 namespace wam {
@@ -12,8 +14,20 @@ using bf16 = __bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
+
+// compile-time loop: f(std::integral_constant<int, 0>) ... f(<N-1>); keeps
+// register-array indices static after inlining
+template <typename F, int... Js>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Js...>) {
+  (f(std::integral_constant<int, Js>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 // ---------------------------------------------------------------- helpers
 __device__ __forceinline__ float to_f32(float x) { return x; }
@@ -52,6 +66,18 @@ enum GemmEpilogue : int {
   EPI_BIAS = 0,       // out[m,n] = acc + bias[n]                       (act type)
   EPI_BIAS_GELU = 1,  // out[m,n] = gelu(acc + bias[n])                 (act type)
   EPI_GATED_RES = 2,  // h[m,n] += gate[n] * (acc + bias[n])            (float32)
+  EPI_QKV = 3,        // q,k RMS-normalised per head -> [B*H][Tpad][64], v -> [B*H][64][Tpad]
+};
+
+// Destination of the QKV epilogue (bf16 mode, head size 64).
+struct QkvOut {
+  bf16* q;
+  bf16* k;
+  bf16* vt;
+  const float* q_g;
+  const float* k_g;
+  int T, Tpad, H, D, qk_norm;
+  float eps;
 };
 
 struct GemmArgs {
@@ -62,8 +88,20 @@ struct GemmArgs {
   void* out;         // [M][N] act type, or float h for EPI_GATED_RES
   int M, N, K;
   int epi;
+  int role;          // distinct kernel symbol per projection (0 qkv, 1 proj, 2 fc1, 3 fc2)
+  float* partial;    // split-K scratch, splits * M * N floats
+  QkvOut qkv;
 };
 
+struct GemmPlan {
+  int cfg;
+  int splits;
+};
+
+GemmPlan plan_gemm(int M, int N, int K, int epi);
+size_t gemm_partial_floats(int M, int N, int K, int epi);
+int gemm_num_configs();
+hipError_t launch_gemm_cfg(const GemmArgs& a, int cfg, int splits, hipStream_t s);
 hipError_t launch_gemm(const GemmArgs& a, bool bf16_mode, hipStream_t s);
 
 // ---------------------------------------------------------------- attention
@@ -75,6 +113,8 @@ struct AttnArgs {
   int B, H, T, Tpad, dh, D;
 };
 hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s);
+// bf16 kernel with qt query tiles of 16 per wave and nw waves per block
+hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, hipStream_t s);
 
 // qkv [B*T][3D] -> q, k (optionally RMS-normalised with gains) and v^T
 struct RelayoutArgs {
@@ -95,7 +135,10 @@ hipError_t launch_qkv_relayout(const RelayoutArgs& a, bool bf16_mode, hipStream_
 // (float or bf16); act: 0 none, 1 SiLU.  partial: float[ceil(K/kc)][N].
 hipError_t launch_gemv(const float* x, const void* W, bool w_bf16, const float* b, float* y,
                        float* partial, int K, int N, int in_act, int out_act, hipStream_t s);
-hipError_t launch_timestep_features(float sigma, float* e, int dim, hipStream_t s);
+// SiLU(c) with c = SiLU(e(sigma) W1 + b1) W2 + b2, e the 256 sinusoidal features
+// (a1: [D] scratch for the hidden layer)
+hipError_t launch_timestep_mlp(float sigma, const float* w1, const float* b1, const float* w2, const float* b2,
+                               float* a1, float* silu_c, int D, hipStream_t s);
 
 struct EmbedArgs {
   const float* x;     // [B][traj]
@@ -116,8 +159,8 @@ struct FinalArgs {
   const float* h;      // [B][T][D]
   const float* shift;  // [D]
   const float* scale;  // [D]
-  const float* wv; const float* bv;  // [D][Cv], [Cv]
-  const float* wa; const float* ba;  // [D][A], [A]
+  const float* wv; const float* bv;  // head weights transposed [Cv][D], bias [Cv]
+  const float* wa; const float* ba;  // [A][D], [A]
   float* v_out;        // [B][traj] or null
   float* x;            // [B][traj] Euler target or null
   float dsigma;        // sigma_{k+1} - sigma_k
@@ -157,7 +200,5 @@ hipError_t launch_remap(const RemapArgs& a, hipStream_t s);
 // Observation Rebinding: sums of ((u_hat-u)/delta)^2 per component, float64
 hipError_t launch_or_sums(int n_comp, const float* const* u_hat, const float* const* u,
                           const int64_t* n, const double* delta, double* sums, hipStream_t s);
-
-hipError_t launch_axpy_copy(const float* src, float* dst, int64_t n, hipStream_t s);
 
 }  // namespace wam

@@ -57,7 +57,7 @@ def test_binding_order_matches_manifest():
 
 
 @pytest.mark.parametrize("bad", [dict(B=0), dict(B=17), dict(D=100), dict(H=5), dict(Na=0),
-                                 dict(dtype="bf16", H=4), dict(Cv=65), dict(ln_eps=0.0)])
+                                 dict(dtype="bf16", H=4), dict(Cv=17), dict(A=17), dict(Co=65), dict(ln_eps=0.0)])
 def test_invalid_configs_rejected(lib, bad):
     base = dict(B=1, L=2, D=128, H=4, F=512, Nv=64, Cv=16, Na=16, A=7, No=8, Co=16, dtype="fp32")
     base.update(bad)
