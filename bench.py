@@ -14,8 +14,12 @@ Prints one JSON line.  --gpus N > 1 is refused: this build runs on one GPU.
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -24,6 +28,88 @@ sys.path.insert(0, ROOT)
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
 HBM_PEAK_GBS = 8000.0
+CLASS_NAMES = ["gemm_qkv", "gemm_proj", "gemm_fc1", "gemm_fc2", "attention", "rr_gate", "rr_inject",
+               "rr_refresh"]
+
+
+def source_hash() -> str:
+    """Hash of the HIP sources; a PMC traffic summary is valid only for these."""
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2609_34608_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode())
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_path(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"pmc_traffic_{workload}.json")
+
+
+def kernel_class(name: str):
+    """Kernel class of a rocprofv3 kernel name (None if not a timed class)."""
+    m = re.search(r"gemm_bf16_kernel<\s*\d+,\s*\d+,\s*\d+,\s*\d+,\s*\d+,\s*\d+,\s*(\d+),", name)
+    if m:
+        return CLASS_NAMES[int(m.group(1))]
+    m = re.search(r"gemm_splitk_reduce_kernel<\s*\d+,\s*(\d+)>", name)  # second pass of a split GEMM
+    if m:
+        return CLASS_NAMES[int(m.group(1))]
+    for key, cls in (("attn_bf16_kernel", "attention"), ("rr_row_sums_kernel", "rr_gate"),
+                     ("rr_finish_kernel", "rr_gate"), ("rr_inject_kernel", "rr_inject"),
+                     ("rr_refresh_kernel", "rr_refresh")):
+        if key in name:
+            return cls
+    return None
+
+
+def summarize_pmc(fetch_csv, write_csv, probe_mb, workload, commands):
+    """Per-class HBM traffic per launch from two rocprofv3 --pmc runs
+    (FETCH_SIZE, WRITE_SIZE), each scaled by what the counter reads for the
+    plain device copy of probe_mb MiB that the same run performs."""
+    def load(path, counter):
+        per = {}
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if r.get("Counter_Name") != counter:
+                    continue
+                per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return per
+    fetch, write = load(fetch_csv, "FETCH_SIZE"), load(write_csv, "WRITE_SIZE")
+    probe_bytes = probe_mb * 2.0 ** 20
+    f_read = probe_bytes / max(fetch.get("__amd_rocclr_copyBuffer", [1.0]))
+    f_write = probe_bytes / max(write.get("__amd_rocclr_copyBuffer", [1.0]))
+    classes = {}
+    for name in set(fetch) | set(write):
+        cls = kernel_class(name)
+        if cls is None:
+            continue
+        fv, wv = fetch.get(name, [0.0]), write.get(name, [0.0])
+        c = classes.setdefault(cls, {"kernels": [], "fetch_counter": 0.0, "write_counter": 0.0})
+        c["kernels"].append(name)
+        c["fetch_counter"] += sum(fv) / len(fv)
+        c["write_counter"] += sum(wv) / len(wv)
+    for c in classes.values():
+        c["traffic_bytes"] = c["fetch_counter"] * f_read + c["write_counter"] * f_write
+    out = {"workload": workload, "source_hash": source_hash(), "probe_mib": probe_mb,
+           "probe_counter": {"FETCH_SIZE": max(fetch.get("__amd_rocclr_copyBuffer", [0.0])),
+                             "WRITE_SIZE": max(write.get("__amd_rocclr_copyBuffer", [0.0]))},
+           "scale": {"read": f_read, "write": f_write}, "commands": commands, "classes": classes}
+    with open(traffic_path(workload), "w") as f:
+        json.dump(out, f, indent=1, sort_keys=True)
+    print(json.dumps({k: round(v["traffic_bytes"]) for k, v in classes.items()}))
+
+
+def lookup_traffic(workload: str, cls: str):
+    """Traffic per launch of a class from the committed PMC summary, or None
+    when there is none or the kernels changed since the counters were taken."""
+    try:
+        with open(traffic_path(workload)) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_hash") != source_hash() or cls not in t.get("classes", {}):
+        return None
+    return t["classes"][cls]["traffic_bytes"]
 
 
 def parse():
@@ -37,11 +123,20 @@ def parse():
     p.add_argument("--cpu-sample-steps", type=int, default=5)
     p.add_argument("--rr-mode", default="auto", choices=["auto", "force_skip", "force_full", "off"],
                    help="residual-rescaling mode of the timed replans")
+    p.add_argument("--copy-probe-mib", type=int, default=0,
+                   help="one plain device copy of this size before timing (PMC calibration)")
+    p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                   help="write the per-class traffic summary of two --pmc runs and exit")
+    p.add_argument("--pmc-command", action="append", default=[], help="command lines recorded in the summary")
     return p.parse_args()
 
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.copy_probe_mib, args.workload,
+                      args.pmc_command)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); multi-GPU runs are not part "
               "of this build.", file=sys.stderr)
@@ -84,6 +179,14 @@ def main():
         return m.replan(cr, x_out, remap_noise[t], cond_pred=cp, u_hat=[cp], u=[cr], delta=[delta],
                         weight=[1.0], noise_first=noise_first, rr=rr, **ra)
 
+    if args.copy_probe_mib:
+        n = args.copy_probe_mib * 2 ** 18
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     torch.cuda.synchronize()
     t = 0
     replan(t)  # first replan: native K steps from noise
@@ -167,7 +270,7 @@ def main():
             "peak": MFMA_BF16_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(dom_tflops / MFMA_BF16_PEAK_TFLOPS, 5),
-            "traffic": None,
+            "traffic": lookup_traffic(spec.name, L.KERNEL_CLASS_NAMES[dom]),
             "launches": dom_n,
             "avg_launch_us": round(1000.0 * dom_ms / dom_n, 3) if dom_n else None,
             "class_ms_one_replan": {L.KERNEL_CLASS_NAMES[k]: round(v, 4) for k, v in tot.items()},

@@ -14,8 +14,11 @@
 // loop is unrolled by PF so that every register slot is static).  Blocks are
 // renumbered so that each XCD (dispatch is round-robin over 8 XCDs) gets a
 // contiguous run of a grouped tile order and shares A rows / W columns in its
-// own L2.  With SPLIT, gridDim.z splits K and fp32 partials go to scratch for a
-// fixed-order second pass.
+// own L2.  With SPLIT, gridDim.z splits K: every split stores an fp32 partial
+// tile and a second pass sums the partials in split order (deterministic) and
+// applies the epilogue.  (A single-kernel variant in which the last-arriving
+// block of a tile does that sum needs agent-scope release/acquire fences, which
+// write back and invalidate the XCD L2s in every block: measured 4-5x slower.)
 #pragma once
 
 #include "wam_internal.h"
@@ -187,6 +190,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
 
   // accumulator (j,i) element r: row m = i*16 + lane%16, column n = j*16 + 4*(lane/16) + r
   if constexpr (SPLIT) {
+    // fp32 partial tile of this K split; the role's reduce pass finishes it
     float* P = a.partial + (size_t)blockIdx.z * a.M * a.N;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
@@ -195,8 +199,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int n = n0 + wn * WN + j * 16 + lg * 4;
-        *reinterpret_cast<float4*>(P + (size_t)m * a.N + n) =
-            make_float4(acc[j][i][0], acc[j][i][1], acc[j][i][2], acc[j][i][3]);
+        *reinterpret_cast<f32x4*>(P + (size_t)m * a.N + n) = acc[j][i];
       }
     }
   } else if constexpr (EPI == EPI_QKV) {
@@ -264,18 +267,15 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
 }
 
 // Split-K second pass: sum the partials in split order, then the epilogue.
-template <int EPI>
+template <int EPI, int ROLE>
 __global__ __launch_bounds__(256) void gemm_splitk_reduce_kernel(GemmArgs a, int splits) {
   const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t n4 = (int64_t)a.M * a.N / 4;
   if (i4 >= n4) return;
   const int m = (int)((i4 * 4) / a.N), n = (int)((i4 * 4) % a.N);
-  float4 s = reinterpret_cast<const float4*>(a.partial)[i4];
-  for (int z = 1; z < splits; ++z) {
-    const float4 p = reinterpret_cast<const float4*>(a.partial + (size_t)z * a.M * a.N)[i4];
-    s.x += p.x; s.y += p.y; s.z += p.z; s.w += p.w;
-  }
-  epi4<EPI>(a, m, n, s.x, s.y, s.z, s.w);
+  f32x4 sum = reinterpret_cast<const f32x4*>(a.partial)[i4];
+  for (int z = 1; z < splits; ++z) sum += reinterpret_cast<const f32x4*>(a.partial + (size_t)z * a.M * a.N)[i4];
+  epi4<EPI>(a, m, n, sum[0], sum[1], sum[2], sum[3]);
 }
 
 template <int BM, int BN, int WGM, int WGN, int PF, int ROLE>
@@ -288,9 +288,9 @@ hipError_t launch_tile(const GemmArgs& a, int splits, hipStream_t s) {
     const int64_t n4 = (int64_t)a.M * a.N / 4;
     const unsigned rb = (unsigned)((n4 + 255) / 256);
     switch (a.epi) {
-      case EPI_BIAS: gemm_splitk_reduce_kernel<EPI_BIAS><<<rb, 256, 0, s>>>(a, splits); break;
-      case EPI_BIAS_GELU: gemm_splitk_reduce_kernel<EPI_BIAS_GELU><<<rb, 256, 0, s>>>(a, splits); break;
-      case EPI_GATED_RES: gemm_splitk_reduce_kernel<EPI_GATED_RES><<<rb, 256, 0, s>>>(a, splits); break;
+      case EPI_BIAS: gemm_splitk_reduce_kernel<EPI_BIAS, ROLE><<<rb, 256, 0, s>>>(a, splits); break;
+      case EPI_BIAS_GELU: gemm_splitk_reduce_kernel<EPI_BIAS_GELU, ROLE><<<rb, 256, 0, s>>>(a, splits); break;
+      case EPI_GATED_RES: gemm_splitk_reduce_kernel<EPI_GATED_RES, ROLE><<<rb, 256, 0, s>>>(a, splits); break;
       default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

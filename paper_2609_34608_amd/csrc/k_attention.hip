@@ -308,6 +308,14 @@ hipError_t launch_qkv_relayout(const RelayoutArgs& a, bool bf16_mode, hipStream_
   return hipGetLastError();
 }
 
+// grid for qt query tiles per wave and nw waves per block
+dim3 grid4(const AttnArgs& a, int qt, int nw) {
+  const int qb = qt * nw * 16;
+  return dim3((a.T + qb - 1) / qb, a.B * a.H);
+}
+
+// (qt, nw) selects the block shape; nw 12 / 14 / 18 are the deep-prefetch
+// variants of (1, 2), (1, 4) and (2, 8) with 7, 7 and 5 K/V tiles in flight.
 hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, hipStream_t s) {
   if (a.dh != kDh || a.Tpad % kKB) return hipErrorInvalidValue;
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)a.dh);
@@ -319,6 +327,9 @@ hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, hipStream_t s
   else if (qt == 4 && nw == 4) attn_bf16_kernel<4, 4, 2><<<grid, 256, 0, s>>>(a, scale_log2);
   else if (qt == 2 && nw == 8) attn_bf16_kernel<2, 8, 3><<<grid, 512, 0, s>>>(a, scale_log2);
   else if (qt == 1 && nw == 8) attn_bf16_kernel<1, 8, 3><<<grid, 512, 0, s>>>(a, scale_log2);
+  else if (qt == 1 && nw == 14) attn_bf16_kernel<1, 4, 7><<<grid4(a, 1, 4), 256, 0, s>>>(a, scale_log2);
+  else if (qt == 1 && nw == 12) attn_bf16_kernel<1, 2, 7><<<grid4(a, 1, 2), 128, 0, s>>>(a, scale_log2);
+  else if (qt == 2 && nw == 18) attn_bf16_kernel<2, 8, 5><<<grid4(a, 2, 8), 512, 0, s>>>(a, scale_log2);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -25,6 +25,8 @@ constexpr TileCfg kCfgs[] = {
     {256, 256, 4, 4, 2},  // 7
     {256, 128, 2, 2, 2},  // 8
     {128, 256, 2, 2, 2},  // 9
+    {256, 256, 2, 2, 2},  // 10
+    {256, 256, 2, 2, 1},  // 11
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
@@ -46,7 +48,9 @@ hipError_t launch_role(const GemmArgs& a, int cfg, int splits, hipStream_t s) {
     case 6: return launch_c<6, ROLE>(a, splits, s);
     case 7: return launch_c<7, ROLE>(a, splits, s);
     case 8: return launch_c<8, ROLE>(a, splits, s);
-    default: return launch_c<9, ROLE>(a, splits, s);
+    case 9: return launch_c<9, ROLE>(a, splits, s);
+    case 10: return launch_c<10, ROLE>(a, splits, s);
+    default: return launch_c<11, ROLE>(a, splits, s);
   }
 }
 

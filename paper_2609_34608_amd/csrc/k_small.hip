@@ -311,21 +311,19 @@ __global__ void rr_row_sums_kernel(const float* __restrict__ hs, const float* __
 
 // One block per (sample, branch): alpha (Eq. crr-alpha), cos and relative
 // fit error (Eq. crr-gate) from the float64 row sums.
-__global__ void rr_finish_kernel(RRGateArgs a) {
+__global__ __launch_bounds__(1024) void rr_finish_kernel(RRGateArgs a) {
   const int b = blockIdx.x / 2, br = blockIdx.x % 2;
   __shared__ double sh[3][16];
   double s[3] = {0.0, 0.0, 0.0};
-  int nrows;
-  if (br == 1) {
-    nrows = a.Na;
-    for (int t = a.Nv + threadIdx.x; t < a.Nv + a.Na; t += blockDim.x)
-      for (int j = 0; j < 3; ++j) s[j] += a.row_sums[((size_t)b * a.T + t) * 3 + j];
-  } else {
-    nrows = a.T - a.Na;
-    for (int i = threadIdx.x; i < nrows; i += blockDim.x) {
-      const int t = i < a.Nv ? i : i + a.Na;
-      for (int j = 0; j < 3; ++j) s[j] += a.row_sums[((size_t)b * a.T + t) * 3 + j];
-    }
+  // branch rows as one index range: A = [Nv, Nv+Na); V = [0, Nv) then [Nv+Na, T)
+  const int nrows = br == 1 ? a.Na : a.T - a.Na;
+  const double* base = a.row_sums + (size_t)b * a.T * 3;
+#pragma unroll 4
+  for (int i = threadIdx.x; i < nrows; i += blockDim.x) {
+    const int t = br == 1 ? a.Nv + i : (i < a.Nv ? i : i + a.Na);
+    s[0] += base[(size_t)t * 3 + 0];
+    s[1] += base[(size_t)t * 3 + 1];
+    s[2] += base[(size_t)t * 3 + 2];
   }
   const int w = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   for (int j = 0; j < 3; ++j) {
@@ -523,7 +521,7 @@ hipError_t launch_rr_gate(const RRGateArgs& a, hipStream_t s) {
   if (a.D % 4) return hipErrorInvalidValue;
   const int wpb = 4;
   rr_row_sums_kernel<<<(rows + wpb - 1) / wpb, wpb * kWave, 0, s>>>(a.hs, a.hq, a.pa, a.row_sums, rows, a.D);
-  rr_finish_kernel<<<a.B * 2, 256, 0, s>>>(a);
+  rr_finish_kernel<<<a.B * 2, 1024, 0, s>>>(a);
   return hipGetLastError();
 }
 
