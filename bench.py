@@ -123,6 +123,8 @@ def parse():
     p.add_argument("--cpu-sample-steps", type=int, default=5)
     p.add_argument("--rr-mode", default="auto", choices=["auto", "force_skip", "force_full", "off"],
                    help="residual-rescaling mode of the timed replans")
+    p.add_argument("--exec", default="host", choices=["host", "device", "graph"],
+                   help="RR decision on the host, on the device, or on the device with graph replay")
     p.add_argument("--copy-probe-mib", type=int, default=0,
                    help="one plain device copy of this size before timing (PMC calibration)")
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -151,7 +153,11 @@ def main():
     spec = get_workload(args.workload)
     dev = torch.device("cuda:0")
     W = make_weights(spec)
-    m = R.WamModel(R.config_of(spec), W, device=dev)
+    m = R.WamModel(R.config_of(spec), W, device=dev, own_stream=args.exec == "graph")
+    if args.exec in ("device", "graph"):
+        m.set_option(L.WAM_OPT_DEVICE_DECISION, 1)
+    if args.exec == "graph":
+        m.set_option(L.WAM_OPT_GRAPHS, 1)
     K = spec.K
     s = np.arange(K + 1, dtype=np.float64)
     sig = (1.0 - s / K)  # uniform flow schedule sigma_k = 1 - k/K
@@ -254,6 +260,7 @@ def main():
                          f"(video {spec.Nv}, action {spec.Na}x{spec.A}, obs {spec.No}) K{spec.K} "
                          f"b0={spec.tr_b0} k1={spec.or_k1} shift={spec.shift_action}"),
             "step": "one replan (control step)",
+            "exec": args.exec,
         },
         "action_chunks_per_s": round(chunks_per_s, 3),
         "denoise_steps_per_replan": n_steps / args.steps,

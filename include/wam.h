@@ -83,6 +83,17 @@ extern "C" {
 #define WAM_PATH_FORCED 3 /* kappa reached kappa_max: refresh, no prefix      */
 #define WAM_PATH_DIRECT 4 /* rebinding disabled: K-b0 steps under c           */
 
+/* ---- wam_set_option ------------------------------------------------------ */
+#define WAM_OPT_DEVICE_DECISION 1 /* 1: the Residual Rescaling decision stays on the
+                                     device; the gate writes a flag that predicates
+                                     the inject / middle / refresh launches, and step
+                                     reports are read back once per call (default 0:
+                                     the host reads the gate and launches one path) */
+#define WAM_OPT_GRAPHS 2          /* 1: wam_replan replays one captured graph per
+                                     (stage, RR variant); needs the device decision
+                                     and a non-default stream; graphs are re-captured
+                                     when the schedule or the RR profile changes */
+
 #define WAM_MAX_BATCH 16
 #define WAM_MAX_COMPONENTS 8
 #define WAM_MAX_STEPS 64
@@ -224,6 +235,10 @@ void wam_destroy(wam_t h);
 int wam_sync(wam_t h);
 const char *wam_last_error(wam_t h);
 const char *wam_status_string(int status);
+/* Execution options (WAM_OPT_*); results are identical either way up to the
+ * order of independent work.  Returns WAM_E_STATE for an invalid combination
+ * and WAM_E_UNSUPPORTED for graphs on the default (null) stream. */
+int wam_set_option(wam_t h, int option, int value);
 
 /* Noise levels sigma_0 = 1 > ... > sigma_K = 0 of the flow schedule
  * (host float[K+1]); K <= WAM_MAX_STEPS.  Required before any step. */

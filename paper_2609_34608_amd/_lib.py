@@ -18,6 +18,7 @@ WAM_RR_OFF, WAM_RR_AUTO, WAM_RR_FORCE_SKIP, WAM_RR_FORCE_FULL = 0, 1, 2, 3
 WAM_ADAPT_REMAP, WAM_ADAPT_RESET_LAYER, WAM_ADAPT_RESET_ALL, WAM_ADAPT_SET_REPLAN = 1, 2, 3, 4
 WAM_PATH_FIRST, WAM_PATH_ACCEPT, WAM_PATH_REJECT, WAM_PATH_FORCED, WAM_PATH_DIRECT = 0, 1, 2, 3, 4
 WAM_MAX_BATCH, WAM_MAX_COMPONENTS, WAM_MAX_STEPS = 16, 8, 64
+WAM_OPT_DEVICE_DECISION, WAM_OPT_GRAPHS = 1, 2
 (WAM_KC_GEMM_QKV, WAM_KC_GEMM_PROJ, WAM_KC_GEMM_FC1, WAM_KC_GEMM_FC2, WAM_KC_ATTENTION,
  WAM_KC_RR_GATE, WAM_KC_RR_INJECT, WAM_KC_RR_REFRESH, WAM_KC_COUNT) = range(9)
 
@@ -84,6 +85,7 @@ EXPORTS = {
     "wam_sync": (C.c_int, [C.c_void_p]),
     "wam_last_error": (C.c_char_p, [C.c_void_p]),
     "wam_status_string": (C.c_char_p, [C.c_int]),
+    "wam_set_option": (C.c_int, [C.c_void_p, C.c_int, C.c_int]),
     "wam_set_schedule": (C.c_int, [C.c_void_p, C.POINTER(C.c_float), C.c_int]),
     "wam_velocity": (C.c_int, [C.c_void_p, C.c_int, C.c_void_p, C.c_void_p, C.c_void_p,
                                C.POINTER(WamRRProfile), C.POINTER(WamStepInfo)]),

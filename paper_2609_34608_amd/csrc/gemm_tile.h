@@ -81,6 +81,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
   static_assert(ACH >= 1 && BCH >= 1 && ACH * NT == BM * 8 && BCH * NT == BN * 8, "tile / thread mismatch");
   static_assert(EPI != EPI_QKV || WN % 64 == 0, "QKV epilogue needs whole heads per wave");
   static_assert(PF >= 1, "prefetch depth");
+  if (a.skip && *a.skip) return;
 
   __shared__ __attribute__((aligned(16))) bf16 As[2][BM][kLds];
   __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN][kLds];
@@ -269,6 +270,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
 // Split-K second pass: sum the partials in split order, then the epilogue.
 template <int EPI, int ROLE>
 __global__ __launch_bounds__(256) void gemm_splitk_reduce_kernel(GemmArgs a, int splits) {
+  if (a.skip && *a.skip) return;
   const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t n4 = (int64_t)a.M * a.N / 4;
   if (i4 >= n4) return;

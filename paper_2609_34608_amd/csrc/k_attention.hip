@@ -26,6 +26,7 @@ namespace {
 // ------------------------------------------------------------- relayout
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void qkv_relayout_kernel(RelayoutArgs a) {
+  if (a.skip && *a.skip) return;
   constexpr int TT = 64;  // tokens per block
   __shared__ float vs[DH][TT + 1];
   const int t0 = blockIdx.x * TT, h = blockIdx.y, b = blockIdx.z;
@@ -74,6 +75,7 @@ constexpr int kVL = kKB + 8;      // LDS row (V^T tile): 64 keys + pad
 
 template <int QT, int NW, int PF>
 __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float scale_log2) {
+  if (a.skip && *a.skip) return;
   constexpr int NT = NW * 64;
   constexpr int QB = NW * QT * 16;  // queries per block
   __shared__ __attribute__((aligned(16))) bf16 Ks[2][kKB][kKL];
@@ -259,6 +261,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
 // One thread per query, online softmax over all keys (parity mode only).
 template <int DH>
 __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
+  if (a.skip && *a.skip) return;
   const int bh = blockIdx.y;
   const int b = bh / a.H, h = bh % a.H;
   const int q = blockIdx.x * 64 + threadIdx.x;

@@ -75,6 +75,7 @@ __device__ __forceinline__ void epi1_f32(const GemmArgs& a, int m, int n, float 
 
 template <int EPI>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
+  if (a.skip && *a.skip) return;
   __shared__ float As[kFK][kFT + 4];
   __shared__ float Bs[kFK][kFT + 4];
   const int m0 = blockIdx.y * kFT, n0 = blockIdx.x * kFT;

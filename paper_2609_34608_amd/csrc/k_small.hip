@@ -146,7 +146,8 @@ __global__ void embed_kernel(EmbedArgs a) {
 template <typename TOut>
 __global__ void ln_modulate_kernel(const float* __restrict__ h, const float* __restrict__ shift,
                                    const float* __restrict__ scale, TOut* __restrict__ u,
-                                   int rows, int D, float eps) {
+                                   int rows, int D, float eps, const int* skip) {
+  if (skip && *skip) return;
   const int row = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   if (row >= rows) return;
@@ -184,7 +185,8 @@ __global__ void ln_modulate_kernel(const float* __restrict__ h, const float* __r
 constexpr int kMaxV4 = 8;  // D <= 2048
 __global__ void ln_modulate_v4_kernel(const float* __restrict__ h, const float* __restrict__ shift,
                                       const float* __restrict__ scale, bf16* __restrict__ u, int rows,
-                                      int D, float eps) {
+                                      int D, float eps, const int* skip) {
+  if (skip && *skip) return;
   const int row = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   if (row >= rows) return;
@@ -362,7 +364,8 @@ __global__ __launch_bounds__(1024) void rr_finish_kernel(RRGateArgs a) {
 // h_e = h_s + alpha_{b,branch} R_a (Eq. residual-injection), in place on h.
 __global__ void rr_inject_kernel(float* __restrict__ h, const float* __restrict__ Ra,
                                  const double* __restrict__ result, int rows, int T, int D,
-                                 int Nv, int Na) {
+                                 int Nv, int Na, const int* flag) {
+  if (flag && *flag != 1) return;
   const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t n4 = (int64_t)rows * D / 4;
   if (i4 >= n4) return;
@@ -380,7 +383,8 @@ __global__ void rr_inject_kernel(float* __restrict__ h, const float* __restrict_
 }
 
 __global__ void rr_pre_middle_kernel(const float* __restrict__ h, float* __restrict__ hq,
-                                     float* __restrict__ pa, int64_t n4) {
+                                     float* __restrict__ pa, int64_t n4, const int* flag) {
+  if (flag && *flag != 0) return;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n4) return;
   const float4 hv = reinterpret_cast<const float4*>(h)[i];
@@ -390,12 +394,36 @@ __global__ void rr_pre_middle_kernel(const float* __restrict__ h, float* __restr
 }
 
 __global__ void rr_refresh_kernel(const float* __restrict__ h, const float* __restrict__ hq,
-                                  float* __restrict__ Ra, int64_t n4) {
+                                  float* __restrict__ Ra, int64_t n4, const int* flag) {
+  if (flag && *flag != 0) return;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n4) return;
   const float4 hv = reinterpret_cast<const float4*>(h)[i];
   const float4 qv = reinterpret_cast<const float4*>(hq)[i];
   reinterpret_cast<float4*>(Ra)[i] = make_float4(hv.x - qv.x, hv.y - qv.y, hv.z - qv.z, hv.w - qv.w);
+}
+
+// Device-side reuse decision: AND of the pass bits over samples and branches
+// (or forced), written as a flag that predicates the following launches.
+__global__ void rr_decide_kernel(const double* __restrict__ result, int B, int force_accept, int* flag,
+                                 double* hist_stats, int* hist_flag) {
+  if (threadIdx.x != 0) return;
+  int all = 1;
+  for (int i = 0; i < B * 2; ++i) {
+    const double* r = result + (size_t)i * 8;
+    all &= r[6] != 0.0;
+    hist_stats[i * 3 + 0] = r[3];
+    hist_stats[i * 3 + 1] = r[4];
+    hist_stats[i * 3 + 2] = r[5];
+  }
+  const int accept = force_accept ? 1 : all;
+  *flag = accept;
+  *hist_flag = accept;
+}
+
+__global__ void copy_f32_kernel(const float* __restrict__ src, float* __restrict__ dst, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[i];
 }
 
 // ------------------------------------------------------------- Trajectory Remapping
@@ -494,16 +522,16 @@ hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_ln_modulate(const float* h, const float* shift, const float* scale, void* u,
-                              int rows, int D, float eps, bool bf16_out, hipStream_t s) {
+                              int rows, int D, float eps, bool bf16_out, hipStream_t s, const int* skip) {
   if (D % kWave || D / kWave > kMaxVpl) return hipErrorInvalidValue;
   const int wpb = 4;
   dim3 grid((rows + wpb - 1) / wpb);
   if (bf16_out && D % 256 == 0)
-    ln_modulate_v4_kernel<<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (bf16*)u, rows, D, eps);
+    ln_modulate_v4_kernel<<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (bf16*)u, rows, D, eps, skip);
   else if (bf16_out)
-    ln_modulate_kernel<bf16><<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (bf16*)u, rows, D, eps);
+    ln_modulate_kernel<bf16><<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (bf16*)u, rows, D, eps, skip);
   else
-    ln_modulate_kernel<float><<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (float*)u, rows, D, eps);
+    ln_modulate_kernel<float><<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (float*)u, rows, D, eps, skip);
   return hipGetLastError();
 }
 
@@ -526,21 +554,35 @@ hipError_t launch_rr_gate(const RRGateArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_rr_inject(float* h, const float* Ra, const double* result, int B, int T, int D,
-                            int Nv, int Na, hipStream_t s) {
+                            int Nv, int Na, hipStream_t s, const int* flag) {
   const int64_t n4 = (int64_t)B * T * D / 4;
-  rr_inject_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(h, Ra, result, B * T, T, D, Nv, Na);
+  rr_inject_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(h, Ra, result, B * T, T, D, Nv, Na, flag);
   return hipGetLastError();
 }
 
-hipError_t launch_rr_pre_middle(const float* h, float* hq, float* pa, int64_t n, hipStream_t s) {
+hipError_t launch_rr_pre_middle(const float* h, float* hq, float* pa, int64_t n, hipStream_t s,
+                                const int* flag) {
   const int64_t n4 = n / 4;
-  rr_pre_middle_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(h, hq, pa, n4);
+  rr_pre_middle_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(h, hq, pa, n4, flag);
   return hipGetLastError();
 }
 
-hipError_t launch_rr_refresh(const float* h, const float* hq, float* Ra, int64_t n, hipStream_t s) {
+hipError_t launch_rr_refresh(const float* h, const float* hq, float* Ra, int64_t n, hipStream_t s,
+                             const int* flag) {
   const int64_t n4 = n / 4;
-  rr_refresh_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(h, hq, Ra, n4);
+  rr_refresh_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(h, hq, Ra, n4, flag);
+  return hipGetLastError();
+}
+
+hipError_t launch_rr_decide(const double* result, int B, int force_accept, int* flag, double* hist_stats,
+                            int* hist_flag, hipStream_t s) {
+  rr_decide_kernel<<<1, 64, 0, s>>>(result, B, force_accept, flag, hist_stats, hist_flag);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  copy_f32_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(src, dst, n);
   return hipGetLastError();
 }
 

@@ -160,6 +160,7 @@ DevLayout dev_layout(const Dims& d) {
 struct WsLayout {
   size_t h, hq, pa, Ra, u, qkv, q, k, vt, attn, mlp, e, a1, sc, mod, gpart, v;
   size_t x_bar, x_r, x_init, x_work, rr_rows, rr_res, tr_rms, or_sums, gsplit, total;
+  size_t rr_flag, hist_stats, hist_flag, cond_buf;
   size_t gpart_floats;
 };
 
@@ -199,6 +200,12 @@ WsLayout ws_layout(const Dims& d) {
     split = std::max(split, gemm_partial_floats(d.M, d.D, d.F, EPI_GATED_RES));
   }
   w.gsplit = take(std::max<size_t>(split, 1) * 4);
+  // device-side reuse decision: flag and one record per stage
+  w.rr_flag = take(4);
+  w.hist_stats = take((size_t)WAM_MAX_STEPS * d.B * 2 * 3 * 8);
+  w.hist_flag = take((size_t)WAM_MAX_STEPS * 4);
+  // condition staging buffer read by captured step graphs
+  w.cond_buf = take((size_t)d.B * d.No * d.Co * 4 + 4);
   w.total = o;
   return w;
 }
@@ -229,6 +236,13 @@ struct wam_handle {
   double* host_stage = nullptr;  // pinned, small
   std::string err;
   ProfSlot prof[WAM_KC_COUNT];
+  bool dev_decision = false;  // RR decision kept on the device (no host round trip per step)
+  bool use_graphs = false;    // replay captured step graphs inside wam_replan
+  bool capturing = false;
+  // captured steps: index k * 3 + variant (0 RR off, 1 establish, 2 attempt)
+  std::vector<hipGraphExec_t> graphs;
+  wam_rr_profile graph_rr{};
+  bool graph_rr_set = false;
 
   template <typename T = float>
   T* W(size_t off) const { return reinterpret_cast<T*>(wdev + off); }
@@ -257,7 +271,7 @@ struct ProfScope {
   bool on;
   ProfScope(wam_t h_, int kc_, double work) : h(h_), kc(kc_), on(false) {
     ProfSlot& p = h->prof[kc];
-    if (p.on && p.used < p.max) {
+    if (p.on && p.used < p.max && !h->capturing) {
       on = true;
       hipEventRecord(p.ev[2 * p.used], h->stream);
       p.work[p.used] = work;
@@ -300,7 +314,7 @@ int embed(wam_t h, const float* x, const float* cond) {
   return WAM_OK;
 }
 
-int run_layer(wam_t h, int l) {
+int run_layer(wam_t h, int l, const int* skip = nullptr) {
   const Dims& d = h->d;
   const DevLayout& wl = h->wl;
   const WsLayout& ws = h->ws;
@@ -322,12 +336,13 @@ int run_layer(wam_t h, int l) {
   float* hh = h->S(ws.h);
   const double M = d.M;
 
-  HIPCHK(h, launch_ln_modulate(hh, mod + 0 * D, mod + 1 * D, h->S<char>(ws.u), d.M, d.D, h->cfg.ln_eps, d.bf, s));
+  HIPCHK(h, launch_ln_modulate(hh, mod + 0 * D, mod + 1 * D, h->S<char>(ws.u), d.M, d.D, h->cfg.ln_eps, d.bf, s,
+                               skip));
   {
     ProfScope ps(h, WAM_KC_GEMM_QKV, 2.0 * M * D * 3 * D);
     GemmArgs g{};
     g.A = h->S<char>(ws.u); g.W = qkv_w; g.bias = qkv_b; g.M = d.M; g.N = (int)(3 * D); g.K = (int)D;
-    g.role = 0; g.partial = h->S(ws.gsplit);
+    g.role = 0; g.partial = h->S(ws.gsplit); g.skip = skip;
     if (d.bf) {
       // projection with q/k RMS-norm and the head-major relayout fused in
       g.epi = EPI_QKV;
@@ -341,40 +356,41 @@ int run_layer(wam_t h, int l) {
   }
   if (!d.bf) {
     RelayoutArgs r{h->S<char>(ws.qkv), q_g, k_g, h->S<char>(ws.q), h->S<char>(ws.k), h->S<char>(ws.vt),
-                   d.B, d.H, d.T, d.Tpad, d.dh, d.D, h->cfg.qk_norm, h->cfg.ln_eps};
+                   d.B, d.H, d.T, d.Tpad, d.dh, d.D, h->cfg.qk_norm, h->cfg.ln_eps, skip};
     HIPCHK(h, launch_qkv_relayout(r, false, s));
   }
   {
     ProfScope ps(h, WAM_KC_ATTENTION, 4.0 * d.B * (double)d.T * d.T * D);
     AttnArgs at{h->S<char>(ws.q), h->S<char>(ws.k), h->S<char>(ws.vt), h->S<char>(ws.attn),
-                d.B, d.H, d.T, d.Tpad, d.dh, d.D};
+                d.B, d.H, d.T, d.Tpad, d.dh, d.D, skip};
     HIPCHK(h, launch_attention(at, d.bf, s));
   }
   {
     ProfScope ps(h, WAM_KC_GEMM_PROJ, 2.0 * M * D * D);
     GemmArgs g{h->S<char>(ws.attn), proj_w, proj_b, mod + 2 * D, hh, d.M, (int)D, (int)D, EPI_GATED_RES, 1,
-               h->S(ws.gsplit), {}};
+               h->S(ws.gsplit), {}, skip};
     HIPCHK(h, launch_gemm(g, d.bf, s));
   }
-  HIPCHK(h, launch_ln_modulate(hh, mod + 3 * D, mod + 4 * D, h->S<char>(ws.u), d.M, d.D, h->cfg.ln_eps, d.bf, s));
+  HIPCHK(h, launch_ln_modulate(hh, mod + 3 * D, mod + 4 * D, h->S<char>(ws.u), d.M, d.D, h->cfg.ln_eps, d.bf, s,
+                               skip));
   {
     ProfScope ps(h, WAM_KC_GEMM_FC1, 2.0 * M * D * d.F);
     GemmArgs g{h->S<char>(ws.u), fc1_w, fc1_b, nullptr, h->S<char>(ws.mlp), d.M, d.F, (int)D, EPI_BIAS_GELU, 2,
-               h->S(ws.gsplit), {}};
+               h->S(ws.gsplit), {}, skip};
     HIPCHK(h, launch_gemm(g, d.bf, s));
   }
   {
     ProfScope ps(h, WAM_KC_GEMM_FC2, 2.0 * M * D * d.F);
     GemmArgs g{h->S<char>(ws.mlp), fc2_w, fc2_b, mod + 5 * D, hh, d.M, (int)D, d.F, EPI_GATED_RES, 3,
-               h->S(ws.gsplit), {}};
+               h->S(ws.gsplit), {}, skip};
     HIPCHK(h, launch_gemm(g, d.bf, s));
   }
   return WAM_OK;
 }
 
-int run_layers(wam_t h, int lo, int hi) {
+int run_layers(wam_t h, int lo, int hi, const int* skip = nullptr) {
   for (int l = lo; l < hi; ++l) {
-    int st = run_layer(h, l);
+    int st = run_layer(h, l, skip);
     if (st) return st;
   }
   return WAM_OK;
@@ -390,8 +406,123 @@ int check_rr(wam_t h, const wam_rr_profile* rr) {
   return WAM_OK;
 }
 
+// Final layer + heads: velocity into v_out and/or Euler update of x_euler.
+int final_step(wam_t h, int k, float* v_out, float* x_euler) {
+  const Dims& d = h->d;
+  FinalArgs f{};
+  const float* fm = h->S(h->ws.mod) + (size_t)d.L * 6 * d.D;
+  f.h = h->S(h->ws.h); f.shift = fm; f.scale = fm + d.D;
+  f.wv = h->W(h->wl.out_wvT); f.bv = h->W(h->wl.out_bv);
+  f.wa = h->W(h->wl.out_waT); f.ba = h->W(h->wl.out_ba);
+  f.v_out = v_out; f.x = x_euler;
+  f.dsigma = (k + 1 <= h->K) ? h->sigmas[k + 1] - h->sigmas[k] : 0.f;
+  f.B = d.B; f.T = d.T; f.D = d.D; f.Nv = d.Nv; f.Cv = d.Cv; f.Na = d.Na; f.A = d.A; f.eps = h->cfg.ln_eps;
+  HIPCHK(h, launch_final(f, h->stream));
+  return WAM_OK;
+}
+
+// One denoising step with the reuse decision taken on the device: the gate
+// writes a flag that the inject (reuse) and the pre-middle / middle-layer /
+// refresh launches (refresh) read, so nothing returns to the host.  Every
+// launch is enqueued whatever the outcome, which also makes the sequence
+// capturable.  attempt: a retained state exists and the mode runs the gate.
+int enqueue_step_device(wam_t h, int k, const float* x, const float* cond, float* v_out, float* x_euler,
+                        const wam_rr_profile* rr, bool attempt) {
+  const Dims& d = h->d;
+  const WsLayout& ws = h->ws;
+  hipStream_t s = h->stream;
+  int st = compute_conditioning(h, h->sigmas[k]);
+  if (st) return st;
+  if ((st = embed(h, x, cond))) return st;
+  float* hh = h->S(ws.h);
+  const int64_t MD = (int64_t)d.M * d.D;
+  if (!rr || rr->mode == WAM_RR_OFF) {
+    if ((st = run_layers(h, 0, d.L))) return st;
+    return final_step(h, k, v_out, x_euler);
+  }
+  if ((st = run_layers(h, 0, rr->q))) return st;
+  HIPCHK(h, launch_copy_f32(hh, h->S(ws.hq), MD, s));
+  if ((st = run_layers(h, rr->q, rr->s))) return st;
+  const int* flag = nullptr;
+  if (attempt) {
+    RRGateArgs g{hh, h->S(ws.hq), h->S(ws.pa), h->S<double>(ws.rr_rows), h->S<double>(ws.rr_res),
+                 d.B, d.T, d.D, d.Nv, d.Na, rr->alpha_min, rr->alpha_max, rr->eps, rr->gamma_cos,
+                 rr->gamma_fit};
+    {
+      ProfScope ps(h, WAM_KC_RR_GATE, 3.0 * MD * 4);
+      HIPCHK(h, launch_rr_gate(g, s));
+    }
+    HIPCHK(h, launch_rr_decide(h->S<double>(ws.rr_res), d.B, rr->mode == WAM_RR_FORCE_SKIP, h->S<int>(ws.rr_flag),
+                               h->S<double>(ws.hist_stats) + (size_t)k * d.B * 6, h->S<int>(ws.hist_flag) + k, s));
+    flag = h->S<int>(ws.rr_flag);
+    {
+      ProfScope ps(h, WAM_KC_RR_INJECT, 3.0 * MD * 4);
+      HIPCHK(h, launch_rr_inject(hh, h->S(ws.Ra), h->S<double>(ws.rr_res), d.B, d.T, d.D, d.Nv, d.Na, s, flag));
+    }
+  }
+  HIPCHK(h, launch_rr_pre_middle(hh, h->S(ws.hq), h->S(ws.pa), MD, s, flag));
+  if ((st = run_layers(h, rr->s, rr->e, flag))) return st;
+  {
+    ProfScope ps(h, WAM_KC_RR_REFRESH, 3.0 * MD * 4);
+    HIPCHK(h, launch_rr_refresh(hh, h->S(ws.hq), h->S(ws.Ra), MD, s, flag));
+  }
+  if ((st = run_layers(h, rr->e, d.L))) return st;
+  return final_step(h, k, v_out, x_euler);
+}
+
+bool same_rr(const wam_rr_profile& a, const wam_rr_profile& b) { return memcmp(&a, &b, sizeof(a)) == 0; }
+
+void drop_graphs(wam_t h) {
+  for (auto& g : h->graphs)
+    if (g) hipGraphExecDestroy(g);
+  h->graphs.clear();
+  h->graph_rr_set = false;
+}
+
+// Device-decision step, replayed from a captured graph when graphs are on and
+// the step reads the internal trajectory / condition buffers (the pointers a
+// graph bakes in).  Capture happens on first use of each (stage, variant).
+int device_step(wam_t h, int k, const float* x, const float* cond, float* x_euler, const wam_rr_profile* rr,
+                bool attempt) {
+  const bool graphable = h->use_graphs && x == h->S(h->ws.x_work) && x_euler == x &&
+                         cond == h->S(h->ws.cond_buf);
+  bool profiling = false;
+  for (auto& p : h->prof) profiling = profiling || p.on;
+  if (!graphable || profiling) return enqueue_step_device(h, k, x, cond, nullptr, x_euler, rr, attempt);
+  const bool active = rr && rr->mode != WAM_RR_OFF;
+  if (active && (!h->graph_rr_set || !same_rr(h->graph_rr, *rr))) {
+    drop_graphs(h);
+    h->graph_rr = *rr;
+    h->graph_rr_set = true;
+  }
+  const int variant = !active ? 0 : (attempt ? 2 : 1);
+  const size_t idx = (size_t)k * 3 + variant;
+  if (h->graphs.size() < (size_t)h->K * 3) h->graphs.resize((size_t)h->K * 3, nullptr);
+  if (!h->graphs[idx]) {
+    hipGraph_t g = nullptr;
+    HIPCHK(h, hipStreamBeginCapture(h->stream, hipStreamCaptureModeThreadLocal));
+    h->capturing = true;
+    int st = enqueue_step_device(h, k, x, cond, nullptr, x_euler, rr, attempt);
+    h->capturing = false;
+    hipError_t e = hipStreamEndCapture(h->stream, &g);
+    if (st) {
+      if (g) hipGraphDestroy(g);
+      return st;
+    }
+    if (e != hipSuccess) return fail(h, WAM_E_HIP, std::string("graph capture: ") + hipGetErrorString(e));
+    hipGraphExec_t ex = nullptr;
+    e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+    hipGraphDestroy(g);
+    if (e != hipSuccess) return fail(h, WAM_E_HIP, std::string("graph instantiate: ") + hipGetErrorString(e));
+    h->graphs[idx] = ex;
+  }
+  HIPCHK(h, hipGraphLaunch(h->graphs[idx], h->stream));
+  return WAM_OK;
+}
+
 // Full forward with Residual Rescaling, then the final layer (velocity into
-// v_out and/or Euler update of x by dsigma).
+// v_out and/or Euler update of x by dsigma).  With the device decision the
+// step info is completed later from the per-stage record (read_history).
 int forward(wam_t h, int k, const float* x, const float* cond, float* v_out, float* x_euler,
             const wam_rr_profile* rr, wam_step_info* info) {
   const Dims& d = h->d;
@@ -401,10 +532,20 @@ int forward(wam_t h, int k, const float* x, const float* cond, float* v_out, flo
   wam_step_info* in = info ? info : &local;
   memset(in, 0, sizeof(*in));
   in->layers_evaluated = d.L;
+  const bool active = rr && rr->mode != WAM_RR_OFF;
+  if (h->dev_decision) {
+    const bool attempt = active && h->layer_valid && (rr->mode == WAM_RR_AUTO || rr->mode == WAM_RR_FORCE_SKIP);
+    in->rr_active = active;
+    in->rr_attempted = attempt;
+    int st = v_out ? enqueue_step_device(h, k, x, cond, v_out, x_euler, rr, attempt)
+                   : device_step(h, k, x, cond, x_euler, rr, attempt);
+    if (st) return st;
+    if (active) h->layer_valid = true;  // either path leaves a valid retained state
+    return WAM_OK;
+  }
   int st = compute_conditioning(h, h->sigmas[k]);
   if (st) return st;
   if ((st = embed(h, x, cond))) return st;
-  const bool active = rr && rr->mode != WAM_RR_OFF;
   float* hh = h->S(ws.h);
   const int64_t MD = (int64_t)d.M * d.D;
   if (!active) {
@@ -412,7 +553,7 @@ int forward(wam_t h, int k, const float* x, const float* cond, float* v_out, flo
   } else {
     in->rr_active = 1;
     if ((st = run_layers(h, 0, rr->q))) return st;
-    HIPCHK(h, hipMemcpyAsync(h->S(ws.hq), hh, MD * 4, hipMemcpyDeviceToDevice, s));
+    HIPCHK(h, launch_copy_f32(hh, h->S(ws.hq), MD, s));
     if ((st = run_layers(h, rr->q, rr->s))) return st;
     bool accept = false;
     if (h->layer_valid && (rr->mode == WAM_RR_AUTO || rr->mode == WAM_RR_FORCE_SKIP)) {
@@ -455,15 +596,38 @@ int forward(wam_t h, int k, const float* x, const float* cond, float* v_out, flo
     }
     if ((st = run_layers(h, rr->e, d.L))) return st;
   }
-  FinalArgs f{};
-  const float* fm = h->S(ws.mod) + (size_t)d.L * 6 * d.D;
-  f.h = hh; f.shift = fm; f.scale = fm + d.D;
-  f.wv = h->W(h->wl.out_wvT); f.bv = h->W(h->wl.out_bv);
-  f.wa = h->W(h->wl.out_waT); f.ba = h->W(h->wl.out_ba);
-  f.v_out = v_out; f.x = x_euler;
-  f.dsigma = (k + 1 <= h->K) ? h->sigmas[k + 1] - h->sigmas[k] : 0.f;
-  f.B = d.B; f.T = d.T; f.D = d.D; f.Nv = d.Nv; f.Cv = d.Cv; f.Na = d.Na; f.A = d.A; f.eps = h->cfg.ln_eps;
-  HIPCHK(h, launch_final(f, s));
+  return final_step(h, k, v_out, x_euler);
+}
+
+// Complete the step infos of stages k_from..k_to-1 from the device record
+// (one copy and one synchronisation per segment).
+int read_history(wam_t h, int k_from, int k_to, const wam_rr_profile* rr, wam_step_info* infos) {
+  if (!h->dev_decision || !infos || k_to <= k_from) return WAM_OK;
+  const Dims& d = h->d;
+  const size_t nst = (size_t)(k_to - k_from) * d.B * 6;
+  std::vector<double> stats(nst);
+  std::vector<int> flags(k_to - k_from);
+  HIPCHK(h, hipMemcpyAsync(stats.data(), h->S<double>(h->ws.hist_stats) + (size_t)k_from * d.B * 6, nst * 8,
+                           hipMemcpyDeviceToHost, h->stream));
+  HIPCHK(h, hipMemcpyAsync(flags.data(), h->S<int>(h->ws.hist_flag) + k_from, flags.size() * 4,
+                           hipMemcpyDeviceToHost, h->stream));
+  HIPCHK(h, hipStreamSynchronize(h->stream));
+  for (int k = k_from; k < k_to; ++k) {
+    wam_step_info& in = infos[k - k_from];
+    if (!in.rr_attempted) continue;
+    const double* st = stats.data() + (size_t)(k - k_from) * d.B * 6;
+    for (int b = 0; b < d.B; ++b)
+      for (int br = 0; br < 2; ++br) {
+        in.alpha[b][br] = st[(b * 2 + br) * 3 + 0];
+        in.cos[b][br] = st[(b * 2 + br) * 3 + 1];
+        in.fit[b][br] = st[(b * 2 + br) * 3 + 2];
+      }
+    if (flags[k - k_from] == 1) {
+      in.rr_accepted = 1;
+      in.layers_skipped = rr->e - rr->s;
+      in.layers_evaluated = d.L - (rr->e - rr->s);
+    }
+  }
   return WAM_OK;
 }
 
@@ -490,8 +654,11 @@ int continue_impl(wam_t h, int k_from, int k_to, float* x, const float* cond, co
     int st = forward(h, k, x, cond, nullptr, x, rr, infos ? &infos[k - k_from] : nullptr);
     if (st) return st;
   }
-  if (capture_stage == k_to && x_capture) return copy_traj(h, x_capture, x);
-  return WAM_OK;
+  if (capture_stage == k_to && x_capture) {
+    int st = copy_traj(h, x_capture, x);
+    if (st) return st;
+  }
+  return read_history(h, k_from, k_to, rr, infos);
 }
 
 }  // namespace
@@ -641,6 +808,7 @@ int wam_init(const wam_config* cfg, const float* hw, size_t n_hw, void* dev_weig
 
 void wam_destroy(wam_t h) {
   if (!h) return;
+  drop_graphs(h);
   for (auto& p : h->prof)
     for (auto ev : p.ev) hipEventDestroy(ev);
   if (h->host_stage) hipHostFree(h->host_stage);
@@ -655,6 +823,24 @@ int wam_sync(wam_t h) {
 
 const char* wam_last_error(wam_t h) { return h ? h->err.c_str() : "null handle"; }
 
+int wam_set_option(wam_t h, int option, int value) {
+  if (!h) return WAM_E_ARG;
+  switch (option) {
+    case WAM_OPT_DEVICE_DECISION:
+      if (!value && h->use_graphs) return fail(h, WAM_E_STATE, "graphs need the device decision");
+      h->dev_decision = value != 0;
+      return WAM_OK;
+    case WAM_OPT_GRAPHS:
+      if (value && !h->dev_decision) return fail(h, WAM_E_STATE, "graphs need the device decision");
+      if (value && h->stream == nullptr) return fail(h, WAM_E_UNSUPPORTED, "graphs need a non-default stream");
+      if (!value) drop_graphs(h);
+      h->use_graphs = value != 0;
+      return WAM_OK;
+    default:
+      return fail(h, WAM_E_ARG, "unknown option");
+  }
+}
+
 int wam_set_schedule(wam_t h, const float* sigmas, int K) {
   if (!h) return WAM_E_ARG;
   if (!sigmas || K < 1 || K > WAM_MAX_STEPS) return fail(h, WAM_E_ARG, "need 1 <= K <= WAM_MAX_STEPS");
@@ -662,6 +848,7 @@ int wam_set_schedule(wam_t h, const float* sigmas, int K) {
     if (!(sigmas[i + 1] < sigmas[i])) return fail(h, WAM_E_ARG, "sigmas must decrease strictly");
   h->sigmas.assign(sigmas, sigmas + K + 1);
   h->K = K;
+  drop_graphs(h);  // captured steps bake the noise levels in
   return WAM_OK;
 }
 
@@ -671,14 +858,16 @@ int wam_velocity(wam_t h, int k, const float* x, const float* cond, float* v_out
   if (st) return st;
   if (!v_out) return fail(h, WAM_E_ARG, "null v_out");
   if ((st = check_rr(h, rr))) return st;
-  return forward(h, k, x, cond, v_out, nullptr, rr, info);
+  if ((st = forward(h, k, x, cond, v_out, nullptr, rr, info))) return st;
+  return read_history(h, k, k + 1, rr, info);
 }
 
 int wam_denoise_step(wam_t h, int k, float* x, const float* cond, const wam_rr_profile* rr, wam_step_info* info) {
   int st = check_step(h, k, x, cond);
   if (st) return st;
   if ((st = check_rr(h, rr))) return st;
-  return forward(h, k, x, cond, nullptr, x, rr, info);
+  if ((st = forward(h, k, x, cond, nullptr, x, rr, info))) return st;
+  return read_history(h, k, k + 1, rr, info);
 }
 
 int wam_continue(wam_t h, int k_from, int k_to, float* x, const float* cond, const wam_rr_profile* rr,
@@ -802,6 +991,11 @@ int wam_replan(wam_t h, const wam_replan_args* a, wam_replan_info* info) {
   int nsteps = 0;
   auto run = [&](int k0, int k1, const float* cond, bool rr_allowed) -> int {
     const wam_rr_profile* rr = (rr_allowed && rr_on) ? &a->rr : nullptr;
+    if (h->use_graphs) {  // captured steps read the condition from the staging buffer
+      float* cb = h->S(h->ws.cond_buf);
+      HIPCHK(h, launch_copy_f32(cond, cb, (int64_t)d.B * d.No * d.Co, h->stream));
+      cond = cb;
+    }
     int st = continue_impl(h, k0, k1, xw, cond, rr, a->r, x_r, steps + nsteps);
     nsteps += k1 - k0;
     return st;

@@ -91,6 +91,7 @@ struct GemmArgs {
   int role;          // distinct kernel symbol per projection (0 qkv, 1 proj, 2 fc1, 3 fc2)
   float* partial;    // split-K scratch, splits * M * N floats
   QkvOut qkv;
+  const int* skip;   // device flag: when non-null and set, the launch does nothing
 };
 
 struct GemmPlan {
@@ -111,6 +112,7 @@ struct AttnArgs {
   const void* vt;  // [B*H][dh][Tpad]
   void* out;       // [B*T][D], head h at columns h*dh
   int B, H, T, Tpad, dh, D;
+  const int* skip; // device flag: when non-null and set, the launch does nothing
 };
 hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s);
 // bf16 kernel with qt query tiles of 16 per wave and nw waves per block
@@ -127,6 +129,7 @@ struct RelayoutArgs {
   int B, H, T, Tpad, dh, D;
   int qk_norm;
   float eps;
+  const int* skip;
 };
 hipError_t launch_qkv_relayout(const RelayoutArgs& a, bool bf16_mode, hipStream_t s);
 
@@ -152,8 +155,10 @@ struct EmbedArgs {
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s);
 
 // u = LN(h) * (1 + scale) + shift  (row-wise over D), u in act type
+// skip: device flag; when non-null and set the launch does nothing
 hipError_t launch_ln_modulate(const float* h, const float* shift, const float* scale, void* u,
-                              int rows, int D, float eps, bool bf16_out, hipStream_t s);
+                              int rows, int D, float eps, bool bf16_out, hipStream_t s,
+                              const int* skip = nullptr);
 
 struct FinalArgs {
   const float* h;      // [B][T][D]
@@ -180,12 +185,23 @@ struct RRGateArgs {
   float alpha_min, alpha_max, eps, gamma_cos, gamma_fit;
 };
 hipError_t launch_rr_gate(const RRGateArgs& a, hipStream_t s);
+// With a device decision flag (1 = reuse, 0 = refresh) the inject runs only on
+// reuse and the pre-middle / refresh passes only on refresh; null = always run.
 hipError_t launch_rr_inject(float* h, const float* Ra, const double* result, int B, int T, int D,
-                            int Nv, int Na, hipStream_t s);
+                            int Nv, int Na, hipStream_t s, const int* flag = nullptr);
 // p_a <- h - hq ; hq <- h   (before recomputing the middle)
-hipError_t launch_rr_pre_middle(const float* h, float* hq, float* pa, int64_t n, hipStream_t s);
+hipError_t launch_rr_pre_middle(const float* h, float* hq, float* pa, int64_t n, hipStream_t s,
+                                const int* flag = nullptr);
 // R_a <- h - hq  (hq holds h_s)
-hipError_t launch_rr_refresh(const float* h, const float* hq, float* Ra, int64_t n, hipStream_t s);
+hipError_t launch_rr_refresh(const float* h, const float* hq, float* Ra, int64_t n, hipStream_t s,
+                             const int* flag = nullptr);
+// Decision on the device: flag = force_accept ? 1 : AND of the (sample, branch)
+// pass bits in result; hist_stats [B][2][3] (alpha, cos, fit) and hist_flag
+// record the step for a later read-back.
+hipError_t launch_rr_decide(const double* result, int B, int force_accept, int* flag, double* hist_stats,
+                            int* hist_flag, hipStream_t s);
+// dst <- src (n floats), a kernel rather than a copy engine command
+hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t s);
 
 // Trajectory Remapping
 struct RemapArgs {

@@ -81,7 +81,8 @@ class StepInfo:
 class WamModel:
     """One libwam handle with its device weights and workspace (torch-owned)."""
 
-    def __init__(self, cfg: abi.WamConfig, weights: dict, device="cuda", stream: torch.cuda.Stream | None = None):
+    def __init__(self, cfg: abi.WamConfig, weights: dict, device="cuda", stream: torch.cuda.Stream | None = None,
+                 own_stream: bool = False):
         if not torch.cuda.is_available():
             raise WamError("libwam needs a HIP device")
         self.lib = abi.lib()
@@ -98,6 +99,8 @@ class WamModel:
                                for n in host_weight_order(cfg.L)])
         if host.size != n_host:
             raise WamError(f"weight count {host.size} != {n_host}")
+        if own_stream:  # a dedicated (default-priority) stream, required for graph replay
+            stream = torch.cuda.Stream(self.device)
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
         self.wdev = torch.empty(wbytes, dtype=torch.uint8, device=self.device)
         self.ws = torch.empty(wsbytes, dtype=torch.uint8, device=self.device)
@@ -111,6 +114,18 @@ class WamModel:
         self.K = 0
 
     # ------------------------------------------------------------ helpers
+    def _enter(self):
+        """Order the handle's stream after torch's current stream (inputs)."""
+        cur = torch.cuda.current_stream(self.device)
+        if cur.cuda_stream != self.stream.cuda_stream:
+            self.stream.wait_stream(cur)
+
+    def _leave(self):
+        """Order torch's current stream after the handle's stream (outputs)."""
+        cur = torch.cuda.current_stream(self.device)
+        if cur.cuda_stream != self.stream.cuda_stream:
+            cur.wait_stream(self.stream)
+
     def _check(self, st, what):
         if st != abi.WAM_OK:
             msg = self.lib.wam_last_error(self.h).decode()
@@ -138,40 +153,50 @@ class WamModel:
         self.K = s.size - 1
 
     def velocity(self, k, x, cond, v_out=None, rr=None):
+        self._enter()
         v_out = self.new_traj() if v_out is None else v_out
         info = abi.WamStepInfo()
         self._check(self.lib.wam_velocity(self.h, k, _ptr(x), _ptr(cond), _ptr(v_out),
                                           C.byref(rr) if rr is not None else None, C.byref(info)),
                     "wam_velocity")
+        self._leave()
         return v_out, StepInfo.of(info, self.B)
 
     def denoise_step(self, k, x, cond, rr=None):
+        self._enter()
         info = abi.WamStepInfo()
         self._check(self.lib.wam_denoise_step(self.h, k, _ptr(x), _ptr(cond),
                                               C.byref(rr) if rr is not None else None, C.byref(info)),
                     "wam_denoise_step")
+        self._leave()
         return StepInfo.of(info, self.B)
 
     def continue_(self, k_from, k_to, x, cond, rr=None, capture_stage=-1, x_capture=None):
+        self._enter()
         n = max(k_to - k_from, 1)
         infos = (abi.WamStepInfo * n)()
         self._check(self.lib.wam_continue(self.h, k_from, k_to, _ptr(x), _ptr(cond),
                                           C.byref(rr) if rr is not None else None, capture_stage,
                                           _ptr(x_capture), infos), "wam_continue")
+        self._leave()
         return [StepInfo.of(infos[i], self.B) for i in range(k_to - k_from)]
 
     def hidden(self, k, x, cond, n_layers, h_out=None):
+        self._enter()
         if h_out is None:
             T = self.cfg.Nv + self.cfg.Na + self.cfg.No
             h_out = torch.empty((self.B, T, self.cfg.D), dtype=torch.float32, device=self.device)
         self._check(self.lib.wam_hidden(self.h, k, _ptr(x), _ptr(cond), n_layers, _ptr(h_out)), "wam_hidden")
+        self._leave()
         return h_out
 
     def remap(self, x_bar, x_r, sigma_r, sigma_b0, shift_action, shift_video, noise, x_out=None):
+        self._enter()
         x_out = self.new_traj() if x_out is None else x_out
         a = abi.WamRemapArgs(x_bar=_ptr(x_bar), x_r=_ptr(x_r), sigma_r=sigma_r, sigma_b0=sigma_b0,
                            shift_action=shift_action, shift_video=shift_video, noise=_ptr(noise), x_out=_ptr(x_out))
         self._check(self.lib.wam_adapt_state(self.h, abi.WAM_ADAPT_REMAP, C.byref(a)), "wam_adapt_state(REMAP)")
+        self._leave()
         return x_out
 
     def reset_layer_state(self):
@@ -181,17 +206,21 @@ class WamModel:
         self._check(self.lib.wam_adapt_state(self.h, abi.WAM_ADAPT_RESET_ALL, None), "RESET_ALL")
 
     def set_replan_state(self, x_bar, x_r, kappa):
+        self._enter()
         a = abi.WamReplanStateArgs(x_bar=_ptr(x_bar), x_r=_ptr(x_r), kappa=kappa)
         self._check(self.lib.wam_adapt_state(self.h, abi.WAM_ADAPT_SET_REPLAN, C.byref(a)), "SET_REPLAN")
 
     def get_replan_state(self):
+        self._enter()
         xb, xr = self.new_traj(), self.new_traj()
         kappa = C.c_int32()
         self._check(self.lib.wam_get_replan_state(self.h, _ptr(xb), _ptr(xr), C.byref(kappa)),
                     "wam_get_replan_state")
+        self._leave()
         return xb, xr, kappa.value
 
     def consistency_score(self, u_hat, u, delta, weight):
+        self._enter()
         n = len(u_hat)
         uh = (C.c_void_p * n)(*[_ptr(t).value for t in u_hat])
         uu = (C.c_void_p * n)(*[_ptr(t).value for t in u])
@@ -201,12 +230,14 @@ class WamModel:
         S = C.c_double()
         self._check(self.lib.wam_consistency_score(self.h, n, uh, uu, cnt, dl, wt, C.byref(S)),
                     "wam_consistency_score")
+        self._leave()
         return S.value
 
     def replan(self, cond_real, x_out, noise_remap, *, cond_pred=None, u_hat=(), u=(), delta=(), weight=(),
                noise_first=None, rr=None, b0=0, r=0, shift_action=0, shift_video=0, k1=0, tau=0.5,
                kappa_max=3, tr_enabled=True, or_enabled=True, rr_first=True, rr_prefix=True,
                rr_refresh=True):
+        self._enter()
         a = abi.WamReplanArgs()
         a.cond_real = _ptr(cond_real)
         a.cond_pred = _ptr(cond_pred)
@@ -227,7 +258,11 @@ class WamModel:
         a.rr_first, a.rr_prefix, a.rr_refresh = int(rr_first), int(rr_prefix), int(rr_refresh)
         info = abi.WamReplanInfo()
         self._check(self.lib.wam_replan(self.h, C.byref(a), C.byref(info)), "wam_replan")
+        self._leave()
         return info
+
+    def set_option(self, option, value):
+        self._check(self.lib.wam_set_option(self.h, option, int(value)), "wam_set_option")
 
     def sync(self):
         self._check(self.lib.wam_sync(self.h), "wam_sync")

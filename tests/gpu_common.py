@@ -44,15 +44,15 @@ def f32_sigmas(K, shift=1.0):
 _MODELS = {}
 
 
-def model_for(name, dev, **wkw):
-    """Cached (spec, weights, WamModel) per workload and weight options."""
+def model_for(name, dev, own_stream=False, **wkw):
+    """Cached (spec, weights, WamModel) per workload, weight options and stream."""
     from paper_2609_34608_amd import runtime as R
-    key = (name, tuple(sorted(wkw.items())))
+    key = (name, own_stream, tuple(sorted(wkw.items())))
     if key not in _MODELS:
         spec = get_workload(name)
         if "B" in wkw:
             spec = spec.replace(B=wkw["B"])
         W = make_weights(spec, **{k: v for k, v in wkw.items() if k != "B"})
-        m = R.WamModel(R.config_of(spec), W, device=dev)
+        m = R.WamModel(R.config_of(spec), W, device=dev, own_stream=own_stream)
         _MODELS[key] = (spec, W, m)
     return _MODELS[key]

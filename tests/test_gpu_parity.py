@@ -26,8 +26,8 @@ def dev():
     return device()
 
 
-def _tiny(dev, name="tiny", B=1):
-    spec, W, m = model_for(name, dev, B=B, bias_std=0.02, gain_std=0.1)
+def _tiny(dev, name="tiny", B=1, own_stream=False):
+    spec, W, m = model_for(name, dev, own_stream=own_stream, B=B, bias_std=0.02, gain_std=0.1)
     sig = f32_sigmas(spec.K)
     m.set_schedule(sig)
     return spec, W, m, sig
@@ -132,6 +132,39 @@ def test_rr_identity_adaptation(dev):
     assert rel_err(v2.cpu().numpy(), v1.cpu().numpy()) <= 1e-5
 
 
+@pytest.mark.parametrize("mode_name", ["AUTO", "FORCE_SKIP", "FORCE_FULL", "NEVER", "MIXED"])
+def test_device_decision_matches_host_decision(dev, mode_name):
+    """The device-resident decision runs the same kernels in the same order:
+    bit-identical trajectories and identical step reports."""
+    from paper_2609_34608_amd import _lib as L
+    spec, W, m, sig = _tiny(dev, "tiny_rr", B=2)
+    modes = {"AUTO": (L.WAM_RR_AUTO, {}), "FORCE_SKIP": (L.WAM_RR_FORCE_SKIP, {}),
+             "FORCE_FULL": (L.WAM_RR_FORCE_FULL, {}), "NEVER": (L.WAM_RR_AUTO, {"gamma_cos": 1.5}),
+             "MIXED": (L.WAM_RR_AUTO, {"gamma_cos": 0.0, "gamma_fit": 1.02})}
+    mode, kw = modes[mode_name]
+    rr_g, rr_o = rr_of(spec, mode, **kw)
+    x0 = make_initial_noise(spec)
+    cond = to_dev(make_observations(spec, 0)[0], dev)
+    outs, infos = [], []
+    for devdec in (0, 1):
+        m.set_option(L.WAM_OPT_DEVICE_DECISION, devdec)
+        m.reset_layer_state()
+        x = to_dev(x0, dev)
+        infos.append(m.continue_(0, spec.K, x, cond, rr=rr_g))
+        outs.append(x.cpu().numpy())
+    m.set_option(L.WAM_OPT_DEVICE_DECISION, 0)
+    np.testing.assert_array_equal(outs[0], outs[1])
+    for a, b in zip(*infos):
+        assert (a.attempted, a.accepted, a.layers_evaluated) == (b.attempted, b.accepted, b.layers_evaluated)
+        np.testing.assert_array_equal(a.alpha, b.alpha)
+        np.testing.assert_array_equal(a.fit, b.fit)
+    # and the forced oracle agrees with the device-decision run
+    trace = deque(i.accepted for i in infos[1] if i.attempted)
+    ref, _, _ = OM.denoise(W, spec, x0, make_observations(spec, 0)[0], sig, 0, spec.K, rr_o, OM.LayerState(),
+                           forced=trace)
+    assert rel_err(outs[1], ref) <= FP32_TOL
+
+
 # ------------------------------------------------------------------ TR and OR
 @pytest.mark.parametrize("shift_a,shift_v", [(0, 0), (3, 0), (5, 7), (16, 0), (20, 64)])
 def test_remap_matches_oracle(dev, shift_a, shift_v):
@@ -163,12 +196,15 @@ def _replan_args(spec):
                 tau=q.or_tau, kappa_max=q.or_kappa_max)
 
 
-@pytest.mark.parametrize("tau", [0.5, 0.3])
-def test_closed_loop_replans_match_oracle(dev, tau):
+@pytest.mark.parametrize("tau,graphs", [(0.5, False), (0.3, False), (0.5, True)])
+def test_closed_loop_replans_match_oracle(dev, tau, graphs):
     """Teacher-forced per replan: the oracle starts from the device's retained
-    state and follows its RR decision trace."""
+    state and follows its RR decision trace.  With graphs, every step is
+    replayed from a captured graph with the decision kept on the device."""
     from paper_2609_34608_amd import _lib as L
-    spec, W, m, sig = _tiny(dev, "tiny_replay")
+    spec, W, m, sig = _tiny(dev, "tiny_replay", own_stream=graphs)
+    m.set_option(L.WAM_OPT_DEVICE_DECISION, int(graphs))
+    m.set_option(L.WAM_OPT_GRAPHS, int(graphs))
     spec = spec.replace(or_tau=tau)
     rr_g, rr_o = rr_of(spec, L.WAM_RR_AUTO)
     ra = _replan_args(spec)
