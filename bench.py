@@ -130,6 +130,10 @@ def parse():
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="write the per-class traffic summary of two --pmc runs and exit")
     p.add_argument("--pmc-command", action="append", default=[], help="command lines recorded in the summary")
+    p.add_argument("--ablation", action="store_true",
+                   help="closed-loop GPU time and observation-to-action latency per variant, then exit")
+    p.add_argument("--window-ms", type=float, default=20.0,
+                   help="simulated action-execution window between replans (ablation mode)")
     return p.parse_args()
 
 
@@ -138,6 +142,11 @@ def main():
     if args.summarize_pmc:
         summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.copy_probe_mib, args.workload,
                       args.pmc_command)
+        return
+    if args.ablation:
+        if args.gpus != 1:
+            sys.exit(2)
+        ablation(args)
         return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); multi-GPU runs are not part "
@@ -325,6 +334,98 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(spec, W, obs, args.cpu_sample_steps)
     print(json.dumps(out), flush=True)
+    m.close()
+
+
+def ablation(args):
+    """Closed-loop replans per variant, mirroring the paper's ablation of the
+    three mechanisms and graph replay: GPU time per replan (foreground +
+    anticipatory, HIP events on the handle's stream) and observation-to-action
+    latency (host clock from the real observation to the ready chunk, Eq.
+    app-o2a).  The anticipatory prefix is enqueued by wam_replan_begin right
+    after the previous chunk and runs during a simulated action window."""
+    import numpy as np
+    import torch
+
+    from paper_2609_34608_amd import _lib as L
+    from paper_2609_34608_amd import runtime as R
+    from synth import get_workload, make_weights, make_initial_noise, make_observations, make_remap_noise
+
+    spec = get_workload(args.workload)
+    dev = torch.device("cuda:0")
+    W = make_weights(spec)
+    m = R.WamModel(R.config_of(spec), W, device=dev, own_stream=True)
+    K = spec.K
+    m.set_schedule(1.0 - np.arange(K + 1) / K)
+    q, s_, e = spec.rr_bounds
+    n = args.warmup + args.steps + 1
+    obs = make_observations(spec, n)
+    rho = spec.ar_rho
+    delta = 1.0 / np.sqrt(1.0 - rho * rho)
+    obs_d = torch.from_numpy(obs).to(dev)
+    pred_d = torch.from_numpy((rho * obs[:-1]).astype(np.float32)).to(dev)
+    noise_first = torch.from_numpy(make_initial_noise(spec)).to(dev)
+    remap_noise = torch.from_numpy(np.stack([make_remap_noise(spec, t) for t in range(n)])).to(dev)
+    x_out = m.new_traj()
+    k2 = K - spec.tr_b0 - spec.or_k1  # steps under the real condition after an accepted prefix
+    variants = [  # name, exec, tr, or, rr mode
+        ("native", "host", False, False, L.WAM_RR_OFF),
+        ("native+graph", "graph", False, False, L.WAM_RR_OFF),
+        ("wamachine", "graph", True, True, L.WAM_RR_AUTO),
+        ("w/o TR", "graph", False, True, L.WAM_RR_AUTO),
+        ("w/o OR", "graph", True, False, L.WAM_RR_AUTO),
+        ("w/o RR", "graph", True, True, L.WAM_RR_OFF),
+        ("w/o graph", "host", True, True, L.WAM_RR_AUTO),
+    ]
+    table = {}
+    for name, ex, tr, orb, rrm in variants:
+        m.set_option(L.WAM_OPT_GRAPHS, 0)
+        m.set_option(L.WAM_OPT_DEVICE_DECISION, int(ex != "host"))
+        m.set_option(L.WAM_OPT_GRAPHS, int(ex == "graph"))
+        rr = R.rr_profile(q, s_, e, rrm, spec.rr_alpha_min, spec.rr_alpha_max, spec.rr_eps, spec.rr_gamma_cos,
+                          spec.rr_gamma_fit)
+        # without remapping the replan enters at stage 0; the prefix then covers
+        # all steps before the last k2, as the paper's w/o-TR variant keeps the
+        # native rebinding stage
+        kw = dict(rr=rr, b0=spec.tr_b0 if tr else 0, r=spec.tr_r, shift_action=spec.shift_action,
+                  shift_video=spec.shift_video, k1=spec.or_k1 if tr else K - k2, tau=spec.or_tau,
+                  kappa_max=spec.or_kappa_max, tr_enabled=tr, or_enabled=orb)
+        m.reset_all()
+        gpu, o2a, steps, infos = [], [], [], []
+        for t in range(n):
+            cp = pred_d[t - 1] if t > 0 else obs_d[t]
+            a = m.replan_args(obs_d[t], x_out, remap_noise[t], cond_pred=cp, u_hat=[cp], u=[obs_d[t]],
+                              delta=[delta], weight=[1.0], noise_first=noise_first, **kw)
+            e0, e1, e2, e3 = (torch.cuda.Event(enable_timing=True) for _ in range(4))
+            e0.record(m.stream)
+            m.replan_begin(a)
+            e1.record(m.stream)
+            time.sleep(args.window_ms * 1e-3)  # action execution; the prefix runs meanwhile
+            t_obs = time.perf_counter()
+            e2.record(m.stream)
+            info = m.replan_end(a)
+            e3.record(m.stream)
+            m.stream.synchronize()
+            t_ready = time.perf_counter()
+            if t > args.warmup:
+                gpu.append(e0.elapsed_time(e1) + e2.elapsed_time(e3))
+                o2a.append(1000.0 * (t_ready - t_obs))
+                steps.append(info.steps)
+                infos.append(info)
+        n_start = sum(i.n_start for i in infos)
+        n_bind = sum(i.n_bind for i in infos)
+        att = sum(i.rr_attempts for i in infos)
+        table[name] = {"gpu_ms": round(float(np.mean(gpu)), 4), "o2a_ms": round(float(np.mean(o2a)), 4),
+                       "steps_per_replan": float(np.mean(steps)),
+                       "or_accept": n_bind / n_start if n_start else None,
+                       "or_coverage": n_bind / len(infos),
+                       "rr_accept": sum(i.rr_reuses for i in infos) / att if att else None}
+    base = table["native"]
+    for v in table.values():
+        v["gpu_speedup"] = round(base["gpu_ms"] / v["gpu_ms"], 3)
+        v["o2a_speedup"] = round(base["o2a_ms"] / v["o2a_ms"], 3)
+    print(json.dumps({"workload": spec.name, "window_ms": args.window_ms, "replans": args.steps,
+                      "variants": table}), flush=True)
     m.close()
 
 

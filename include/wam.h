@@ -278,6 +278,17 @@ int wam_consistency_score(wam_t h, int n_components, const float *const *u_hat,
  * and rebinding or restart, with Residual Rescaling inside each step.  The
  * retained replan state (x_bar, x^r, kappa) lives in the workspace. */
 int wam_replan(wam_t h, const wam_replan_args *args, wam_replan_info *info);
+/* The same replan in two halves, so that the anticipatory prefix overlaps
+ * action execution (Sec. 3.2).  wam_replan_begin applies Trajectory Remapping
+ * and enqueues the prefix under cond_pred; with WAM_OPT_DEVICE_DECISION it
+ * returns without waiting for the GPU.  wam_replan_end, called once the real
+ * observation is available, computes the consistency score, rebinds or
+ * restarts under cond_real, and fills info.  Both take the same args (the
+ * buffers must stay valid until wam_replan_end returns); wam_replan_end
+ * without a begin runs the whole replan.  A second begin before end is
+ * WAM_E_STATE. */
+int wam_replan_begin(wam_t h, const wam_replan_args *args);
+int wam_replan_end(wam_t h, const wam_replan_args *args, wam_replan_info *info);
 /* Copies of the retained replan state (device [B][traj] each; may be NULL). */
 int wam_get_replan_state(wam_t h, float *x_bar, float *x_r, int32_t *kappa);
 

@@ -99,6 +99,8 @@ EXPORTS = {
                                         C.POINTER(C.c_int64), C.POINTER(C.c_double), C.POINTER(C.c_double),
                                         C.POINTER(C.c_double)]),
     "wam_replan": (C.c_int, [C.c_void_p, C.POINTER(WamReplanArgs), C.POINTER(WamReplanInfo)]),
+    "wam_replan_begin": (C.c_int, [C.c_void_p, C.POINTER(WamReplanArgs)]),
+    "wam_replan_end": (C.c_int, [C.c_void_p, C.POINTER(WamReplanArgs), C.POINTER(WamReplanInfo)]),
     "wam_get_replan_state": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.POINTER(C.c_int32)]),
     "wam_profile_enable": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int]),
     "wam_profile_read": (C.c_int, [C.c_void_p, C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int64),

@@ -243,6 +243,16 @@ struct wam_handle {
   std::vector<hipGraphExec_t> graphs;
   wam_rr_profile graph_rr{};
   bool graph_rr_set = false;
+  // replan split into begin (remap + anticipatory prefix) and end
+  struct Pending {
+    bool begun = false;
+    bool first = false;   // no retained state: the whole replan runs in end
+    bool prefix = false;  // prefix enqueued, its step reports not yet read back
+    int entry = 0;
+    int nsteps = 0;
+    wam_step_info steps[WAM_MAX_STEPS * 2];
+    wam_replan_info info;
+  } pend;
 
   template <typename T = float>
   T* W(size_t off) const { return reinterpret_cast<T*>(wdev + off); }
@@ -645,7 +655,7 @@ int copy_traj(wam_t h, float* dst, const float* src) {
 }
 
 int continue_impl(wam_t h, int k_from, int k_to, float* x, const float* cond, const wam_rr_profile* rr,
-                  int capture_stage, float* x_capture, wam_step_info* infos) {
+                  int capture_stage, float* x_capture, wam_step_info* infos, bool read_back = true) {
   for (int k = k_from; k < k_to; ++k) {
     if (capture_stage == k && x_capture) {
       int st = copy_traj(h, x_capture, x);
@@ -658,7 +668,7 @@ int continue_impl(wam_t h, int k_from, int k_to, float* x, const float* cond, co
     int st = copy_traj(h, x_capture, x);
     if (st) return st;
   }
-  return read_history(h, k_from, k_to, rr, infos);
+  return read_back ? read_history(h, k_from, k_to, rr, infos) : WAM_OK;
 }
 
 }  // namespace
@@ -915,6 +925,7 @@ int wam_adapt_state(wam_t h, int op, const void* args) {
       h->layer_valid = false;
       h->has_prev = false;
       h->kappa = 0;
+      h->pend.begun = false;
       return WAM_OK;
     case WAM_ADAPT_SET_REPLAN: {
       const wam_replan_state_args* a = static_cast<const wam_replan_state_args*>(args);
@@ -956,8 +967,11 @@ int wam_consistency_score(wam_t h, int n, const float* const* u_hat, const float
   return WAM_OK;
 }
 
-int wam_replan(wam_t h, const wam_replan_args* a, wam_replan_info* info) {
-  if (!h) return WAM_E_ARG;
+}  // extern "C"
+
+namespace {
+
+int check_replan_args(wam_t h, const wam_replan_args* a) {
   if (!a || !a->cond_real || !a->x_out || !a->noise_remap) return fail(h, WAM_E_ARG, "null replan argument");
   if (h->K <= 0) return fail(h, WAM_E_STATE, "schedule not set (wam_set_schedule)");
   const int K = h->K;
@@ -970,90 +984,132 @@ int wam_replan(wam_t h, const wam_replan_args* a, wam_replan_info* info) {
     if (!a->cond_pred) return fail(h, WAM_E_ARG, "rebinding needs cond_pred");
     if (a->kappa_max < 0) return fail(h, WAM_E_ARG, "kappa_max must be >= 0");
   }
-  const bool rr_on = a->rr.mode != WAM_RR_OFF;
-  if (rr_on) {
+  if (a->rr.mode != WAM_RR_OFF) {
     int st = check_rr(h, &a->rr);
     if (st) return st;
   }
   if (!h->has_prev && !a->noise_first) return fail(h, WAM_E_ARG, "first replan needs noise_first");
+  return WAM_OK;
+}
 
-  wam_replan_info loc{};
-  wam_replan_info* inf = info ? info : &loc;
-  memset(inf, 0, sizeof(*inf));
-  inf->S = -1.0;
-  for (int i = 0; i < WAM_MAX_STEPS; ++i) inf->decision[i] = -1;
+// Steps k0..k1-1 on the working trajectory, recording their reports in the
+// pending replan; the latent at the retained stage r is captured on the way.
+int run_segment(wam_t h, const wam_replan_args* a, int k0, int k1, const float* cond, bool rr_allowed,
+                bool read_back) {
   const Dims& d = h->d;
-  float* x_bar = h->S(h->ws.x_bar);
-  float* x_r = h->S(h->ws.x_r);
-  float* x_init = h->S(h->ws.x_init);
-  float* xw = h->S(h->ws.x_work);
-  wam_step_info steps[WAM_MAX_STEPS * 2];
-  int nsteps = 0;
-  auto run = [&](int k0, int k1, const float* cond, bool rr_allowed) -> int {
-    const wam_rr_profile* rr = (rr_allowed && rr_on) ? &a->rr : nullptr;
-    if (h->use_graphs) {  // captured steps read the condition from the staging buffer
-      float* cb = h->S(h->ws.cond_buf);
-      HIPCHK(h, launch_copy_f32(cond, cb, (int64_t)d.B * d.No * d.Co, h->stream));
-      cond = cb;
-    }
-    int st = continue_impl(h, k0, k1, xw, cond, rr, a->r, x_r, steps + nsteps);
-    nsteps += k1 - k0;
-    return st;
-  };
-  int st;
-  h->layer_valid = false;  // layer state is scoped to one replan
-  if (!h->has_prev) {
-    if ((st = copy_traj(h, xw, a->noise_first))) return st;
-    if ((st = run(0, K, a->cond_real, a->rr_first))) return st;
-    inf->path = WAM_PATH_FIRST;
-  } else {
-    if (a->tr_enabled) {
-      RemapArgs r{x_bar, x_r, a->noise_remap, x_init, h->S<double>(h->ws.tr_rms), h->sigmas[a->r],
-                  h->sigmas[a->b0], a->shift_action, a->shift_video, d.B, d.Nv, d.Cv, d.Na, d.A};
-      HIPCHK(h, launch_remap(r, h->stream));
-    } else {
-      if ((st = copy_traj(h, x_init, a->noise_remap))) return st;
-    }
-    if ((st = copy_traj(h, xw, x_init))) return st;
-    if (a->or_enabled && h->kappa < a->kappa_max) {
-      inf->n_start = 1;
-      if ((st = run(entry, entry + a->k1, a->cond_pred, a->rr_prefix))) return st;
-      double S = 0.0;
-      st = wam_consistency_score(h, a->n_components, a->u_hat, a->u, a->n, a->delta, a->weight, &S);
-      if (st) return st;
-      inf->S = S;
-      if (S < a->tau && h->kappa < a->kappa_max) {
-        h->kappa += 1;
-        inf->n_bind = 1;
-        inf->path = WAM_PATH_ACCEPT;
-        if ((st = run(entry + a->k1, K, a->cond_real, a->rr_prefix))) return st;
-      } else {
-        h->kappa = 0;
-        inf->path = WAM_PATH_REJECT;
-        h->layer_valid = false;
-        if ((st = copy_traj(h, xw, x_init))) return st;
-        if ((st = run(entry, K, a->cond_real, a->rr_refresh))) return st;
-      }
-    } else {
-      inf->path = a->or_enabled ? WAM_PATH_FORCED : WAM_PATH_DIRECT;
-      if (a->or_enabled) h->kappa = 0;
-      if ((st = run(entry, K, a->cond_real, a->rr_refresh))) return st;
-    }
+  const wam_rr_profile* rr = (rr_allowed && a->rr.mode != WAM_RR_OFF) ? &a->rr : nullptr;
+  if (h->use_graphs) {  // captured steps read the condition from the staging buffer
+    float* cb = h->S(h->ws.cond_buf);
+    HIPCHK(h, launch_copy_f32(cond, cb, (int64_t)d.B * d.No * d.Co, h->stream));
+    cond = cb;
   }
-  if ((st = copy_traj(h, x_bar, xw))) return st;
+  int st = continue_impl(h, k0, k1, h->S(h->ws.x_work), cond, rr, a->r, h->S(h->ws.x_r),
+                         h->pend.steps + h->pend.nsteps, read_back);
+  h->pend.nsteps += k1 - k0;
+  return st;
+}
+
+}  // namespace
+
+extern "C" {
+
+int wam_replan_begin(wam_t h, const wam_replan_args* a) {
+  if (!h) return WAM_E_ARG;
+  int st = check_replan_args(h, a);
+  if (st) return st;
+  if (h->pend.begun) return fail(h, WAM_E_STATE, "replan already begun (call wam_replan_end)");
+  auto& p = h->pend;
+  p.first = p.prefix = false;
+  p.nsteps = 0;
+  memset(&p.info, 0, sizeof(p.info));
+  p.info.S = -1.0;
+  for (int i = 0; i < WAM_MAX_STEPS; ++i) p.info.decision[i] = -1;
+  p.entry = a->tr_enabled ? a->b0 : 0;
+  h->layer_valid = false;  // layer state is scoped to one replan
+  p.begun = true;
+  if (!h->has_prev) {
+    p.first = true;  // nothing to anticipate without a previous replan
+    return WAM_OK;
+  }
+  const Dims& d = h->d;
+  float* x_init = h->S(h->ws.x_init);
+  if (a->tr_enabled) {
+    RemapArgs r{h->S(h->ws.x_bar), h->S(h->ws.x_r), a->noise_remap, x_init, h->S<double>(h->ws.tr_rms),
+                h->sigmas[a->r], h->sigmas[a->b0], a->shift_action, a->shift_video, d.B, d.Nv, d.Cv, d.Na, d.A};
+    HIPCHK(h, launch_remap(r, h->stream));
+  } else {
+    if ((st = copy_traj(h, x_init, a->noise_remap))) return st;
+  }
+  if ((st = copy_traj(h, h->S(h->ws.x_work), x_init))) return st;
+  if (a->or_enabled && h->kappa < a->kappa_max) {
+    p.info.n_start = 1;
+    p.prefix = true;
+    if ((st = run_segment(h, a, p.entry, p.entry + a->k1, a->cond_pred, a->rr_prefix, false))) return st;
+  }
+  return WAM_OK;
+}
+
+int wam_replan_end(wam_t h, const wam_replan_args* a, wam_replan_info* info) {
+  if (!h) return WAM_E_ARG;
+  int st;
+  if (!h->pend.begun && (st = wam_replan_begin(h, a))) return st;
+  if ((st = check_replan_args(h, a))) return st;
+  auto& p = h->pend;
+  p.begun = false;
+  const Dims& d = h->d;
+  const int K = h->K;
+  float* xw = h->S(h->ws.x_work);
+  wam_replan_info* inf = &p.info;
+  if (p.first) {
+    if ((st = copy_traj(h, xw, a->noise_first))) return st;
+    if ((st = run_segment(h, a, 0, K, a->cond_real, a->rr_first, true))) return st;
+    inf->path = WAM_PATH_FIRST;
+  } else if (p.prefix) {
+    const wam_rr_profile* rrp = (a->rr_prefix && a->rr.mode != WAM_RR_OFF) ? &a->rr : nullptr;
+    if ((st = read_history(h, p.entry, p.entry + a->k1, rrp, p.steps))) return st;
+    double S = 0.0;
+    st = wam_consistency_score(h, a->n_components, a->u_hat, a->u, a->n, a->delta, a->weight, &S);
+    if (st) return st;
+    inf->S = S;
+    if (S < a->tau && h->kappa < a->kappa_max) {
+      h->kappa += 1;
+      inf->n_bind = 1;
+      inf->path = WAM_PATH_ACCEPT;
+      if ((st = run_segment(h, a, p.entry + a->k1, K, a->cond_real, a->rr_prefix, true))) return st;
+    } else {
+      h->kappa = 0;
+      inf->path = WAM_PATH_REJECT;
+      h->layer_valid = false;
+      if ((st = copy_traj(h, xw, h->S(h->ws.x_init)))) return st;
+      if ((st = run_segment(h, a, p.entry, K, a->cond_real, a->rr_refresh, true))) return st;
+    }
+  } else {
+    inf->path = a->or_enabled ? WAM_PATH_FORCED : WAM_PATH_DIRECT;
+    if (a->or_enabled) h->kappa = 0;
+    if ((st = run_segment(h, a, p.entry, K, a->cond_real, a->rr_refresh, true))) return st;
+  }
+  if ((st = copy_traj(h, h->S(h->ws.x_bar), xw))) return st;
   if ((st = copy_traj(h, a->x_out, xw))) return st;
   h->has_prev = true;
   inf->kappa = h->kappa;
-  inf->steps = nsteps;
-  for (int i = 0; i < nsteps; ++i) {
-    const wam_step_info& s = steps[i];
+  inf->steps = p.nsteps;
+  for (int i = 0; i < p.nsteps; ++i) {
+    const wam_step_info& s = p.steps[i];
     if (i < WAM_MAX_STEPS) inf->decision[i] = s.rr_attempted ? (int8_t)s.rr_accepted : (int8_t)-1;
     inf->rr_attempts += s.rr_attempted;
     inf->rr_reuses += s.rr_accepted;
     inf->layers_skipped += s.layers_skipped;
     if (s.rr_active) inf->layers_dense += d.L;
   }
+  if (info) *info = *inf;
   return WAM_OK;
+}
+
+int wam_replan(wam_t h, const wam_replan_args* a, wam_replan_info* info) {
+  if (!h) return WAM_E_ARG;
+  int st = wam_replan_begin(h, a);
+  if (st) return st;
+  return wam_replan_end(h, a, info);
 }
 
 int wam_get_replan_state(wam_t h, float* xb, float* xr, int32_t* kappa) {

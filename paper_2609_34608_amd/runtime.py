@@ -233,11 +233,11 @@ class WamModel:
         self._leave()
         return S.value
 
-    def replan(self, cond_real, x_out, noise_remap, *, cond_pred=None, u_hat=(), u=(), delta=(), weight=(),
-               noise_first=None, rr=None, b0=0, r=0, shift_action=0, shift_video=0, k1=0, tau=0.5,
-               kappa_max=3, tr_enabled=True, or_enabled=True, rr_first=True, rr_prefix=True,
-               rr_refresh=True):
-        self._enter()
+    def replan_args(self, cond_real, x_out, noise_remap, *, cond_pred=None, u_hat=(), u=(), delta=(), weight=(),
+                    noise_first=None, rr=None, b0=0, r=0, shift_action=0, shift_video=0, k1=0, tau=0.5,
+                    kappa_max=3, tr_enabled=True, or_enabled=True, rr_first=True, rr_prefix=True,
+                    rr_refresh=True):
+        """The wam_replan_args struct (device buffers referenced, not copied)."""
         a = abi.WamReplanArgs()
         a.cond_real = _ptr(cond_real)
         a.cond_pred = _ptr(cond_pred)
@@ -256,8 +256,25 @@ class WamModel:
         a.tau, a.kappa_max = tau, kappa_max
         a.tr_enabled, a.or_enabled = int(tr_enabled), int(or_enabled)
         a.rr_first, a.rr_prefix, a.rr_refresh = int(rr_first), int(rr_prefix), int(rr_refresh)
+        return a
+
+    def replan(self, cond_real, x_out, noise_remap, **kw):
+        self._enter()
+        a = self.replan_args(cond_real, x_out, noise_remap, **kw)
         info = abi.WamReplanInfo()
         self._check(self.lib.wam_replan(self.h, C.byref(a), C.byref(info)), "wam_replan")
+        self._leave()
+        return info
+
+    def replan_begin(self, args):
+        """Remap and enqueue the anticipatory prefix (args from replan_args)."""
+        self._enter()
+        self._check(self.lib.wam_replan_begin(self.h, C.byref(args)), "wam_replan_begin")
+
+    def replan_end(self, args):
+        self._enter()
+        info = abi.WamReplanInfo()
+        self._check(self.lib.wam_replan_end(self.h, C.byref(args), C.byref(info)), "wam_replan_end")
         self._leave()
         return info
 

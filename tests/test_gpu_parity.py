@@ -287,3 +287,41 @@ def test_full_size_layer_sampled_rows(dev, name, layers):
         e = rel_err(upd_got, upd_ref)
         print(f"{name} layer {l} sampled-row update rel err {e:.3e}")
         assert e <= BF16_TOL, (l, e)
+
+
+def test_split_replan_matches_one_call(dev):
+    """wam_replan_begin (remap + prefix enqueued without waiting) followed by
+    wam_replan_end equals wam_replan, replan by replan, bit for bit."""
+    from paper_2609_34608_amd import _lib as L
+    spec, W, m, sig = _tiny(dev, "tiny_replay", own_stream=True)
+    m.set_option(L.WAM_OPT_GRAPHS, 0)
+    m.set_option(L.WAM_OPT_DEVICE_DECISION, 1)
+    rr_g, _ = rr_of(spec, L.WAM_RR_AUTO, gamma_cos=0.0, gamma_fit=1.02)
+    ra = _replan_args(spec)
+    rho = spec.ar_rho
+    delta = 1.0 / np.sqrt(1 - rho * rho)
+    obs = make_observations(spec, spec.control_steps)
+    runs = []
+    for split in (False, True):
+        m.reset_all()
+        x_out = m.new_traj()
+        outs, paths = [], []
+        for t in range(spec.control_steps):
+            cr = to_dev(obs[t], dev)
+            cp = to_dev((rho * obs[t - 1]).astype(np.float32) if t > 0 else obs[t], dev)
+            kw = dict(cond_pred=cp, u_hat=[cp], u=[cr], delta=[delta], weight=[1.0],
+                      noise_first=to_dev(make_initial_noise(spec), dev), rr=rr_g, **ra)
+            noise = to_dev(make_remap_noise(spec, t), dev)
+            if split:
+                a = m.replan_args(cr, x_out, noise, **kw)
+                m.replan_begin(a)
+                info = m.replan_end(a)
+            else:
+                info = m.replan(cr, x_out, noise, **kw)
+            outs.append(x_out.cpu().numpy())
+            paths.append((info.path, info.steps, info.kappa, list(info.decision[:info.steps])))
+        runs.append((outs, paths))
+    m.set_option(L.WAM_OPT_DEVICE_DECISION, 0)
+    assert runs[0][1] == runs[1][1]
+    for a, b in zip(runs[0][0], runs[1][0]):
+        np.testing.assert_array_equal(a, b)
