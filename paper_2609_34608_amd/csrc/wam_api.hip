@@ -645,7 +645,7 @@ int check_step(wam_t h, int k, const void* x, const void* cond) {
   if (!h) return WAM_E_ARG;
   if (h->K <= 0) return fail(h, WAM_E_STATE, "schedule not set (wam_set_schedule)");
   if (k < 0 || k >= h->K) return fail(h, WAM_E_ARG, "step index out of range");
-  if (!x || !cond) return fail(h, WAM_E_ARG, "null trajectory or condition pointer");
+  if (!x || (!cond && h->d.No > 0)) return fail(h, WAM_E_ARG, "null trajectory or condition pointer");
   return WAM_OK;
 }
 
@@ -885,7 +885,7 @@ int wam_continue(wam_t h, int k_from, int k_to, float* x, const float* cond, con
   if (!h) return WAM_E_ARG;
   if (h->K <= 0) return fail(h, WAM_E_STATE, "schedule not set (wam_set_schedule)");
   if (k_from < 0 || k_to > h->K || k_from > k_to) return fail(h, WAM_E_ARG, "need 0 <= k_from <= k_to <= K");
-  if (!x || !cond) return fail(h, WAM_E_ARG, "null trajectory or condition pointer");
+  if (!x || (!cond && h->d.No > 0)) return fail(h, WAM_E_ARG, "null trajectory or condition pointer");
   int st = check_rr(h, rr);
   if (st) return st;
   return continue_impl(h, k_from, k_to, x, cond, rr, capture_stage, x_capture, infos);
@@ -972,7 +972,8 @@ int wam_consistency_score(wam_t h, int n, const float* const* u_hat, const float
 namespace {
 
 int check_replan_args(wam_t h, const wam_replan_args* a) {
-  if (!a || !a->cond_real || !a->x_out || !a->noise_remap) return fail(h, WAM_E_ARG, "null replan argument");
+  if (!a || (!a->cond_real && h->d.No > 0) || !a->x_out || !a->noise_remap)
+    return fail(h, WAM_E_ARG, "null replan argument");
   if (h->K <= 0) return fail(h, WAM_E_STATE, "schedule not set (wam_set_schedule)");
   const int K = h->K;
   if (a->b0 < 0 || a->b0 >= K) return fail(h, WAM_E_ARG, "need 0 <= b0 < K");
@@ -981,7 +982,7 @@ int check_replan_args(wam_t h, const wam_replan_args* a) {
   const int entry = a->tr_enabled ? a->b0 : 0;
   if (a->or_enabled) {
     if (!(0 < a->k1 && a->k1 < K - entry)) return fail(h, WAM_E_ARG, "need 0 < k1 < K - b0");
-    if (!a->cond_pred) return fail(h, WAM_E_ARG, "rebinding needs cond_pred");
+    if (!a->cond_pred && h->d.No > 0) return fail(h, WAM_E_ARG, "rebinding needs cond_pred");
     if (a->kappa_max < 0) return fail(h, WAM_E_ARG, "kappa_max must be >= 0");
   }
   if (a->rr.mode != WAM_RR_OFF) {

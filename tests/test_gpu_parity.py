@@ -325,3 +325,66 @@ def test_split_replan_matches_one_call(dev):
     assert runs[0][1] == runs[1][1]
     for a, b in zip(runs[0][0], runs[1][0]):
         np.testing.assert_array_equal(a, b)
+
+
+# ------------------------------------------------------------------ edge cases
+@pytest.mark.parametrize("shape", [dict(Nv=0), dict(No=0), dict(Na=1, A=1), dict(B=16, Nv=24, No=3),
+                                   dict(Nv=63, No=1)])
+def test_degenerate_shapes_chunk_matches_oracle(dev, shape):
+    """No video tokens, no observation tokens, a one-slot one-dim action
+    chunk, the maximum batch, and ragged T: native chunk within 1e-4."""
+    from paper_2609_34608_amd import runtime as R
+    spec = get_workload("tiny").replace(**shape)
+    W = make_weights(spec, bias_std=0.02)
+    m = R.WamModel(R.config_of(spec), W, device=dev)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    x = to_dev(x0, dev)
+    m.continue_(0, spec.K, x, to_dev(cond, dev))
+    ref, _, _ = OM.denoise(W, spec, x0, cond, sig, 0, spec.K, None, OM.LayerState())
+    assert rel_err(x.cpu().numpy(), ref) <= FP32_TOL
+    m.close()
+
+
+def test_kappa_max_zero_always_refreshes(dev):
+    """kappa_max = 0: no prefix is ever started; every replan refreshes from
+    the remapped initialisation (FORCED path), K - b0 steps."""
+    from paper_2609_34608_amd import _lib as L
+    spec, W, m, sig = _tiny(dev, "tiny_replay")
+    m.set_option(L.WAM_OPT_GRAPHS, 0)
+    m.set_option(L.WAM_OPT_DEVICE_DECISION, 0)
+    ra = dict(_replan_args(spec), kappa_max=0)
+    obs = make_observations(spec, 3)
+    m.reset_all()
+    x_out = m.new_traj()
+    for t in range(4):
+        c = to_dev(obs[t], dev)
+        info = m.replan(c, x_out, to_dev(make_remap_noise(spec, t), dev), cond_pred=c, u_hat=[c], u=[c],
+                        delta=[1.0], weight=[1.0], noise_first=to_dev(make_initial_noise(spec), dev), **ra)
+        if t > 0:
+            assert info.path == L.WAM_PATH_FORCED and info.n_start == 0 and info.steps == spec.K - spec.tr_b0
+            assert info.S == -1.0
+
+
+def test_error_returns(dev):
+    """Invalid arguments return an error status and leave the handle usable."""
+    from paper_2609_34608_amd import _lib as L
+    from paper_2609_34608_amd.runtime import WamError, rr_profile
+    spec, W, m, sig = _tiny(dev, "tiny_rr")
+    x = to_dev(make_initial_noise(spec), dev)
+    c = to_dev(make_observations(spec, 0)[0], dev)
+    with pytest.raises(WamError, match="sigma_r"):
+        m.remap(x, x.clone(), 0.0, 0.5, 0, 0, x.clone())
+    with pytest.raises(WamError, match="shifts"):
+        m.remap(x, x.clone(), 0.5, 0.5, -1, 0, x.clone())
+    with pytest.raises(WamError, match="0 < q < s < e < L"):
+        m.velocity(0, x, c, rr=rr_profile(2, 2, 3, L.WAM_RR_AUTO))
+    with pytest.raises(WamError, match="step index"):
+        m.velocity(spec.K, x, c)
+    with pytest.raises(WamError, match="strictly"):
+        m.set_schedule(np.array([1.0, 0.5, 0.5, 0.0]))
+    m.set_schedule(sig)
+    v, _ = m.velocity(0, x, c)  # still usable
+    assert torch.isfinite(v).all()
