@@ -103,14 +103,14 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
   }
   const int nk = (kend - kbeg) / kBK;
 
-  // per-thread global offsets (row clamped so that the zero-filled tail rows stay in bounds)
+  // per-thread global offsets; tile rows past M read row M-1 instead (their
+  // products only reach output rows that are never stored, and loading
+  // unmasked keeps the prefetch free of waits on its own data)
   const bf16* pa[ACH];
-  bool va[ACH];
 #pragma unroll
   for (int i = 0; i < ACH; ++i) {
     const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
-    va[i] = m0 + row < a.M;
-    pa[i] = A + (size_t)(va[i] ? m0 + row : 0) * K + kbeg + col;
+    pa[i] = A + (size_t)min(m0 + row, a.M - 1) * K + kbeg + col;
   }
   const bf16* pw[BCH];
 #pragma unroll
@@ -123,10 +123,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
   auto gload = [&](auto S, int kt) __attribute__((always_inline)) {
     constexpr int slot = decltype(S)::value;
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const u32x4 v = *reinterpret_cast<const u32x4*>(pa[i] + kt * kBK);
-      ra[slot][i] = va[i] ? v : u32x4{0u, 0u, 0u, 0u};
-    }
+    for (int i = 0; i < ACH; ++i) ra[slot][i] = *reinterpret_cast<const u32x4*>(pa[i] + kt * kBK);
 #pragma unroll
     for (int i = 0; i < BCH; ++i) rb[slot][i] = *reinterpret_cast<const u32x4*>(pw[i] + kt * kBK);
   };
@@ -175,19 +172,31 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
   });
   sstore(std::integral_constant<int, 0>{}, 0);
   __syncthreads();
-  // steady state, unrolled by PF: register slot of tile t is t % PF, LDS buffer t % 2
-  for (int kt0 = 0; kt0 < nk; kt0 += PF) {
+  // steady state, unrolled by PF: register slot of tile t is t % PF, LDS
+  // buffer t % 2.  Full groups of PF tiles run branch-free (the prefetch index
+  // is clamped to the last tile, and a store after the last tile lands in the
+  // buffer nobody reads again), so the compiler's wait counts stay exact and
+  // PF tiles really are in flight; only the last partial group branches.
+  const int nfull = nk / PF * PF;
+  for (int kt0 = 0; kt0 < nfull; kt0 += PF) {
     static_for<PF>([&](auto J) __attribute__((always_inline)) {
       constexpr int j = decltype(J)::value;
       const int kt = kt0 + j;
-      if (kt < nk) {
-        if (kt + PF < nk) gload(J, kt + PF);  // slot j held tile kt, already in LDS
-        compute(kt & 1);
-        if (kt + 1 < nk) sstore(std::integral_constant<int, (j + 1) % PF>{}, (kt + 1) & 1);
-        __syncthreads();
-      }
+      gload(J, min(kt + PF, nk - 1));  // slot j held tile kt, already in LDS
+      compute(kt & 1);
+      sstore(std::integral_constant<int, (j + 1) % PF>{}, (kt + 1) & 1);
+      __syncthreads();
     });
   }
+  static_for<PF>([&](auto J) __attribute__((always_inline)) {
+    constexpr int j = decltype(J)::value;
+    const int kt = nfull + j;
+    if (kt < nk) {
+      compute(kt & 1);
+      if (kt + 1 < nk) sstore(std::integral_constant<int, (j + 1) % PF>{}, (kt + 1) & 1);
+      __syncthreads();
+    }
+  });
 
   // accumulator (j,i) element r: row m = i*16 + lane%16, column n = j*16 + 4*(lane/16) + r
   if constexpr (SPLIT) {

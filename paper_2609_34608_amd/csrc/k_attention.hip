@@ -138,7 +138,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
     }
   };
 
-  auto block = [&](int buf, int k0) __attribute__((always_inline)) {
+  auto block = [&](int buf, int k0, auto MASK) __attribute__((always_inline)) {
     // S^T tiles [key tile kt][query tile qt]
     f32x4 s[4][QT];
 #pragma unroll
@@ -152,15 +152,17 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
         s[kt][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1f, qf[qt][1], z, 0, 0, 0);
       }
     }
-    // mask keys >= T (key of element r: k0 + kt*16 + 4g + r)
-    if (k0 + kKB > a.T) {
+    // mask keys >= T (key of element r: k0 + kt*16 + 4g + r); only the last
+    // key tile can hold such keys, so only its instance carries the mask
+    if constexpr (decltype(MASK)::value) {
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (k0 + kt * 16 + g * 4 + r >= a.T)
+        for (int r = 0; r < 4; ++r) {
+          const bool live = k0 + kt * 16 + g * 4 + r < a.T;
 #pragma unroll
-            for (int qt = 0; qt < QT; ++qt) s[kt][qt][r] = -INFINITY;
+          for (int qt = 0; qt < QT; ++qt) s[kt][qt][r] = live ? s[kt][qt][r] : -INFINITY;
+        }
     }
     // online softmax per query column (lane-local except the max)
     bf16x8 pf[2][QT];
@@ -223,18 +225,34 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
   });
   sstore(std::integral_constant<int, 0>{}, 0);
   __syncthreads();
-  for (int kb0 = 0; kb0 < nkb; kb0 += PF) {
+  // Full groups of PF tiles run branch-free (prefetch index clamped to the
+  // last tile; a store after the last tile goes to a buffer nobody reads
+  // again) so that PF tiles stay in flight.  The last tile is kept out of the
+  // groups: it runs last, with the key mask.
+  const std::integral_constant<bool, false> nomask{};
+  const std::integral_constant<bool, true> withmask{};
+  const int nbody = nkb - 1;
+  const int nfull = nbody / PF * PF;
+  for (int kb0 = 0; kb0 < nfull; kb0 += PF) {
     static_for<PF>([&](auto J) __attribute__((always_inline)) {
       constexpr int j = decltype(J)::value;
       const int kb = kb0 + j;
-      if (kb < nkb) {
-        if (kb + PF < nkb) gload(J, (kb + PF) * kKB);  // slot j held tile kb, already in LDS
-        block(kb & 1, kb * kKB);
-        if (kb + 1 < nkb) sstore(std::integral_constant<int, (j + 1) % PF>{}, (kb + 1) & 1);
-        __syncthreads();
-      }
+      gload(J, min(kb + PF, nkb - 1) * kKB);  // slot j held tile kb, already in LDS
+      block(kb & 1, kb * kKB, nomask);
+      sstore(std::integral_constant<int, (j + 1) % PF>{}, (kb + 1) & 1);
+      __syncthreads();
     });
   }
+  static_for<PF>([&](auto J) __attribute__((always_inline)) {
+    constexpr int j = decltype(J)::value;
+    const int kb = nfull + j;
+    if (kb < nbody) {
+      block(kb & 1, kb * kKB, nomask);
+      sstore(std::integral_constant<int, (j + 1) % PF>{}, (kb + 1) & 1);
+      __syncthreads();
+    }
+  });
+  block(nbody & 1, nbody * kKB, withmask);
 
   // normalise and store O[b*T + q][h*64 + dh]; lane holds dh = d*16 + 4g + r of query lr
   bf16* out = static_cast<bf16*>(a.out);
@@ -312,37 +330,36 @@ hipError_t launch_qkv_relayout(const RelayoutArgs& a, bool bf16_mode, hipStream_
 }
 
 // grid for qt query tiles per wave and nw waves per block
-dim3 grid4(const AttnArgs& a, int qt, int nw) {
-  const int qb = qt * nw * 16;
-  return dim3((a.T + qb - 1) / qb, a.B * a.H);
-}
-
-// (qt, nw) selects the block shape; nw 12 / 14 / 18 are the deep-prefetch
-// variants of (1, 2), (1, 4) and (2, 8) with 7, 7 and 5 K/V tiles in flight.
-hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, hipStream_t s) {
+// (qt, nw, pf): query tiles of 16 per wave, waves per block, K/V tiles in
+// flight.  Only the instantiated combinations are accepted.
+hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int pf, hipStream_t s) {
   if (a.dh != kDh || a.Tpad % kKB) return hipErrorInvalidValue;
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)a.dh);
   const int qb = qt * nw * 16;
-  dim3 grid((a.T + qb - 1) / qb, a.B * a.H);
-  if (qt == 1 && nw == 2) attn_bf16_kernel<1, 2, 3><<<grid, 128, 0, s>>>(a, scale_log2);
-  else if (qt == 1 && nw == 4) attn_bf16_kernel<1, 4, 3><<<grid, 256, 0, s>>>(a, scale_log2);
-  else if (qt == 2 && nw == 4) attn_bf16_kernel<2, 4, 3><<<grid, 256, 0, s>>>(a, scale_log2);
-  else if (qt == 4 && nw == 4) attn_bf16_kernel<4, 4, 2><<<grid, 256, 0, s>>>(a, scale_log2);
-  else if (qt == 2 && nw == 8) attn_bf16_kernel<2, 8, 3><<<grid, 512, 0, s>>>(a, scale_log2);
-  else if (qt == 1 && nw == 8) attn_bf16_kernel<1, 8, 3><<<grid, 512, 0, s>>>(a, scale_log2);
-  else if (qt == 1 && nw == 14) attn_bf16_kernel<1, 4, 7><<<grid4(a, 1, 4), 256, 0, s>>>(a, scale_log2);
-  else if (qt == 1 && nw == 12) attn_bf16_kernel<1, 2, 7><<<grid4(a, 1, 2), 128, 0, s>>>(a, scale_log2);
-  else if (qt == 2 && nw == 18) attn_bf16_kernel<2, 8, 5><<<grid4(a, 2, 8), 512, 0, s>>>(a, scale_log2);
-  else return hipErrorInvalidValue;
+  const dim3 grid((a.T + qb - 1) / qb, a.B * a.H);
+  const int key = qt * 10000 + nw * 100 + pf;
+  switch (key) {
+    case 10203: attn_bf16_kernel<1, 2, 3><<<grid, 128, 0, s>>>(a, scale_log2); break;
+    case 10207: attn_bf16_kernel<1, 2, 7><<<grid, 128, 0, s>>>(a, scale_log2); break;
+    case 10403: attn_bf16_kernel<1, 4, 3><<<grid, 256, 0, s>>>(a, scale_log2); break;
+    case 10407: attn_bf16_kernel<1, 4, 7><<<grid, 256, 0, s>>>(a, scale_log2); break;
+    case 10803: attn_bf16_kernel<1, 8, 3><<<grid, 512, 0, s>>>(a, scale_log2); break;
+    case 20403: attn_bf16_kernel<2, 4, 3><<<grid, 256, 0, s>>>(a, scale_log2); break;
+    case 20803: attn_bf16_kernel<2, 8, 3><<<grid, 512, 0, s>>>(a, scale_log2); break;
+    case 20805: attn_bf16_kernel<2, 8, 5><<<grid, 512, 0, s>>>(a, scale_log2); break;
+    case 40402: attn_bf16_kernel<4, 4, 2><<<grid, 256, 0, s>>>(a, scale_log2); break;
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s) {
   if (bf16_mode) {
-    // 8 waves x 32 queries when that still fills the chip, else 4 waves x 16
+    // 8 waves x 32 queries with 5 K/V tiles in flight when that still fills
+    // the chip, else 4 waves x 16 queries
     const long blocks = (long)((a.T + 255) / 256) * a.B * a.H;
-    if (blocks >= 256) return launch_attention_cfg(a, 2, 8, s);
-    return launch_attention_cfg(a, 1, 4, s);
+    if (blocks >= 256) return launch_attention_cfg(a, 2, 8, 5, s);
+    return launch_attention_cfg(a, 1, 4, 3, s);
   }
   dim3 grid((a.T + 63) / 64, a.B * a.H);
   if (a.dh == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(a);

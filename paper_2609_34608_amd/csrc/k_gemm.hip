@@ -22,11 +22,12 @@ constexpr TileCfg kCfgs[] = {
     {128, 128, 2, 4, 4},  // 4
     {256, 128, 4, 2, 3},  // 5
     {128, 256, 2, 4, 3},  // 6
-    {256, 256, 4, 4, 2},  // 7
+    {256, 256, 4, 4, 1},  // 7
     {256, 128, 2, 2, 2},  // 8
     {128, 256, 2, 2, 2},  // 9
-    {256, 256, 2, 2, 2},  // 10
+    {256, 128, 4, 2, 4},  // 10
     {256, 256, 2, 2, 1},  // 11
+    {128, 256, 2, 4, 4},  // 12
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
@@ -50,6 +51,7 @@ hipError_t launch_role(const GemmArgs& a, int cfg, int splits, hipStream_t s) {
     case 8: return launch_c<8, ROLE>(a, splits, s);
     case 9: return launch_c<9, ROLE>(a, splits, s);
     case 10: return launch_c<10, ROLE>(a, splits, s);
+    case 12: return launch_c<12, ROLE>(a, splits, s);
     default: return launch_c<11, ROLE>(a, splits, s);
   }
 }
@@ -125,9 +127,11 @@ int gemm_num_configs() { return kNumCfgs; }
 
 GemmPlan plan_gemm(int M, int N, int K, int epi) {
   // Chosen from a sweep of every tile configuration at the workload shapes:
-  // the 256x256 tile with 16 waves wins whenever M gives ~8+ tile rows; below
-  // that, 64x64 tiles (64x128 for the QKV epilogue, which needs whole heads
-  // per wave), with K split into >= 768-deep slices while that adds blocks.
+  // 256x256 tiles with 16 waves (64x64 each, one K tile in flight, four waves
+  // per SIMD) once M gives enough tile rows; below that 64x64 tiles (64x128
+  // for the QKV epilogue, which needs whole heads per wave).  With K tiles in
+  // flight the small-M shapes no longer gain from splitting K; a split is kept
+  // for grids under half a block per CU.
   GemmPlan p{0, 1};
   if (M >= 2048 && N % 256 == 0) {
     p.cfg = 7;
@@ -138,7 +142,7 @@ GemmPlan plan_gemm(int M, int N, int K, int epi) {
     return p;
   }
   const long blocks = (long)((M + 63) / 64) * (N / 64);
-  while (blocks * p.splits < 384 && K / (p.splits * 2) >= 768 && K % (gemm::kBK * p.splits * 2) == 0 &&
+  while (blocks * p.splits < 128 && K / (p.splits * 2) >= 768 && K % (gemm::kBK * p.splits * 2) == 0 &&
          p.splits < 8)
     p.splits *= 2;
   return p;

@@ -116,7 +116,7 @@ struct AttnArgs {
 };
 hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s);
 // bf16 kernel with qt query tiles of 16 per wave and nw waves per block
-hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, hipStream_t s);
+hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int pf, hipStream_t s);
 
 // qkv [B*T][3D] -> q, k (optionally RMS-normalised with gains) and v^T
 struct RelayoutArgs {
