@@ -28,6 +28,10 @@ COMMON = [
     f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17",
     # packed fp32 instructions are kept out of generated code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators stay in architectural VGPRs: with the default
+    # heuristic, unrolled loops shuffle accumulators between AGPRs and VGPRs
+    # with several copy instructions per MFMA
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wno-unused-result", f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 
