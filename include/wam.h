@@ -98,7 +98,7 @@ extern "C" {
 #define WAM_MAX_COMPONENTS 8
 #define WAM_MAX_STEPS 64
 
-/* Kernel classes for wam_profile_* (per-launch HIP-event timing). */
+/* Kernel classes for wam_profile_* (per-launch timing from dispatch timestamps). */
 #define WAM_KC_GEMM_QKV 0
 #define WAM_KC_GEMM_PROJ 1
 #define WAM_KC_GEMM_FC1 2
@@ -293,8 +293,11 @@ int wam_replan_end(wam_t h, const wam_replan_args *args, wam_replan_info *info);
 int wam_get_replan_state(wam_t h, float *x_bar, float *x_r, int32_t *kappa);
 
 /* ---- measurement ------------------------------------------------------------ */
-/* Record a HIP event pair around every launch of kernel class kc (WAM_KC_*),
- * up to max_launches launches, on the handle's stream.  enable = 0 stops. */
+/* Time every launch of kernel class kc (WAM_KC_*), up to max_launches
+ * launches: a HIP event pair per launch, stamped by the dispatches themselves
+ * (begin of the class's first kernel, end of its last; hipExtLaunchKernel), so
+ * no event packets sit between the timed kernels.  Launches inside a graph
+ * capture are not timed.  enable = 0 stops. */
 int wam_profile_enable(wam_t h, int kc, int enable, int max_launches);
 /* Sum of launch durations (ms), launch count and algorithmic work (FLOP for
  * contractions, bytes for streaming kernels) of the recorded launches.

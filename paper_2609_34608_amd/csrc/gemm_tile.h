@@ -6,19 +6,23 @@
 // activation tile as its second, so accumulator element r of a lane is
 // C[m = lane%16][n = 4*(lane/16) + r]: each lane owns four consecutive output
 // columns of one row and the epilogue stores 8 (bf16) or 16 (fp32) contiguous
-// bytes.  A block of WGM x WGN waves owns a BM x BN tile.  K advances 64 at a
-// time through a double-buffered LDS ring whose rows are padded to 72 bf16 (the
-// 16 rows one MFMA operand read touches fall in distinct banks).  The ring is
-// fed from registers that hold the next PF K tiles: loads for tile kt+PF are
-// issued while tile kt is multiplied, so PF tiles are in flight per block (the
-// loop is unrolled by PF so that every register slot is static).  Blocks are
-// renumbered so that each XCD (dispatch is round-robin over 8 XCDs) gets a
-// contiguous run of a grouped tile order and shares A rows / W columns in its
-// own L2.  With SPLIT, gridDim.z splits K: every split stores an fp32 partial
-// tile and a second pass sums the partials in split order (deterministic) and
-// applies the epilogue.  (A single-kernel variant in which the last-arriving
-// block of a tile does that sum needs agent-scope release/acquire fences, which
-// write back and invalidate the XCD L2s in every block: measured 4-5x slower.)
+// bytes.  A block of WGM x WGN waves owns a BM x BN tile.
+//
+// K advances 32 at a time through ST LDS stages.  Each stage holds BM
+// activation rows and BN weight rows of 64 bytes, filled straight from global
+// memory by global_load_lds_dwordx4 (16 bytes per lane, one 1 KiB run of LDS
+// per instruction, no register staging): ST-1 stages are in flight while one
+// is multiplied.  Inside a row the four 16-byte chunks are XOR-swizzled by
+// (row >> 1) & 3, which keeps the ds_read_b128 operand reads (16 rows x one
+// chunk per 16 lanes) free of bank conflicts; the loads pick their global
+// chunk so that the LDS image comes out swizzled.  The compiler cannot follow
+// the LDS writes of these loads, so the loop waits on vmcnt itself and uses a
+// bare s_barrier (a workgroup fence would drain every load in flight).
+// Blocks are renumbered so that each XCD (dispatch is round-robin over 8 XCDs)
+// gets a contiguous run of a grouped tile order and shares A rows / W columns
+// in its own L2.  With SPLIT, gridDim.z splits K: every split stores an fp32
+// partial tile and a second pass sums the partials in split order
+// (deterministic) and applies the epilogue.
 #pragma once
 
 #include "wam_internal.h"
@@ -26,11 +30,23 @@
 namespace wam {
 namespace gemm {
 
-constexpr int kBK = 64;
-constexpr int kPad = 8;
-constexpr int kLds = kBK + kPad;  // bf16 elements per LDS row
+constexpr int kBK = 32;    // K per stage: one 64-byte LDS row
 constexpr int kGroupM = 8;
 constexpr int kXcd = 8;
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void global_void;
+
+// s_waitcnt immediate (gfx9 layout: vmcnt bits 3:0 and 15:14, expcnt 6:4,
+// lgkmcnt 11:8): at most n vector-memory operations outstanding, no LDS or
+// scalar-memory operation outstanding
+constexpr int waitcnt_vm_lgkm0(int n) { return (n & 0xf) | ((n >> 4) << 14) | (0x7 << 4); }
+
+// swizzled 16-byte chunk of a 64-byte LDS row
+__device__ __forceinline__ int chunk_swizzle(int row) { return (row >> 1) & 3; }
+
+// compiler-only memory barrier: keeps LDS and global accesses on their side
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
 
 __device__ __forceinline__ void tile_coords(int bid, int nblocks, int tiles_m, int tiles_n, int& tm,
                                             int& tn) {
@@ -70,21 +86,21 @@ __device__ __forceinline__ void epi4(const GemmArgs& a, int m, int n, float v0, 
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int PF, int EPI, int ROLE, bool SPLIT>
+template <int BM, int BN, int WGM, int WGN, int ST, int EPI, int ROLE, bool SPLIT>
 __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
-  constexpr int NT = WGM * WGN * 64;
+  constexpr int NW = WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN;  // wave tile
   constexpr int TM = WM / 16, TN = WN / 16;
-  constexpr int ACH = BM * (kBK / 8) / NT;  // 16-byte chunks per thread per K tile
-  constexpr int BCH = BN * (kBK / 8) / NT;
+  constexpr int ROWS = BM + BN;                // LDS rows per stage: activations, then weights
+  constexpr int NI = ROWS / 16;                // 1 KiB load instructions per stage
+  constexpr int IPW = NI / NW;                 // ... per wave
   static_assert(TM >= 1 && TN >= 1, "wave tile too small");
-  static_assert(ACH >= 1 && BCH >= 1 && ACH * NT == BM * 8 && BCH * NT == BN * 8, "tile / thread mismatch");
+  static_assert(IPW >= 1 && IPW * NW == NI, "stage rows / wave mismatch");
   static_assert(EPI != EPI_QKV || WN % 64 == 0, "QKV epilogue needs whole heads per wave");
-  static_assert(PF >= 1, "prefetch depth");
+  static_assert(ST >= 2 && (ST - 2) * IPW < 64, "stage count");
   if (a.skip && *a.skip) return;
 
-  __shared__ __attribute__((aligned(16))) bf16 As[2][BM][kLds];
-  __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN][kLds];
+  __shared__ __attribute__((aligned(1024))) bf16 sm[ST][ROWS * kBK];
 
   const int tiles_m = (a.M + BM - 1) / BM, tiles_n = a.N / BN;
   int tm, tn;
@@ -97,48 +113,30 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
   const int K = a.K;
   int kbeg = 0, kend = K;
   if constexpr (SPLIT) {
-    const int per = K / gridDim.z;  // host guarantees divisibility by 64 * splits
+    const int per = K / gridDim.z;  // host guarantees divisibility by kBK * splits
     kbeg = blockIdx.z * per;
     kend = kbeg + per;
   }
   const int nk = (kend - kbeg) / kBK;
 
-  // per-thread global offsets; tile rows past M read row M-1 instead (their
-  // products only reach output rows that are never stored, and loading
-  // unmasked keeps the prefetch free of waits on its own data)
-  const bf16* pa[ACH];
+  // Load instruction j of this wave fills LDS rows 16*(wid + NW*j) .. +15;
+  // lane l writes LDS chunk l%4 of row l/4, i.e. global chunk (l%4) ^ swizzle.
+  // Activation rows past M read row M-1 (their products reach only output
+  // rows that are never stored).
+  const bf16* src[IPW];
 #pragma unroll
-  for (int i = 0; i < ACH; ++i) {
-    const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
-    pa[i] = A + (size_t)min(m0 + row, a.M - 1) * K + kbeg + col;
+  for (int j = 0; j < IPW; ++j) {
+    const int row = 16 * (wid + NW * j) + lane / 4;
+    const int col = ((lane % 4) ^ chunk_swizzle(row)) * 8;
+    src[j] = row < BM ? A + (size_t)min(m0 + row, a.M - 1) * K + kbeg + col
+                      : W + (size_t)(n0 + row - BM) * K + kbeg + col;
   }
-  const bf16* pw[BCH];
+  auto issue = [&](auto S, int kt) __attribute__((always_inline)) {
+    constexpr int s = decltype(S)::value;
 #pragma unroll
-  for (int i = 0; i < BCH; ++i) {
-    const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
-    pw[i] = W + (size_t)(n0 + row) * K + kbeg + col;
-  }
-
-  u32x4 ra[PF][ACH], rb[PF][BCH];
-  auto gload = [&](auto S, int kt) __attribute__((always_inline)) {
-    constexpr int slot = decltype(S)::value;
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) ra[slot][i] = *reinterpret_cast<const u32x4*>(pa[i] + kt * kBK);
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) rb[slot][i] = *reinterpret_cast<const u32x4*>(pw[i] + kt * kBK);
-  };
-  auto sstore = [&](auto S, int buf) __attribute__((always_inline)) {
-    constexpr int slot = decltype(S)::value;
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
-      *reinterpret_cast<u32x4*>(&As[buf][row][col]) = ra[slot][i];
-    }
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
-      *reinterpret_cast<u32x4*>(&Bs[buf][row][col]) = rb[slot][i];
-    }
+    for (int j = 0; j < IPW; ++j)
+      __builtin_amdgcn_global_load_lds((const global_void*)(src[j] + kt * kBK),
+                                       (lds_void*)(&sm[s][(wid + NW * j) * 16 * kBK]), 16, 0, 0);
   };
 
   f32x4 acc[TN][TM];
@@ -147,56 +145,50 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < TM; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int lr = lane % 16, lg = lane / 16, lk = lg * 8;
-  auto compute = [&](int buf) __attribute__((always_inline)) {
+  // operand reads: lane (lr, lg) takes chunk lg of row lr of each 16-row tile
+  // (tile row offsets are multiples of 16, so the swizzle depends on lr only)
+  const int lr = lane % 16, lg = lane / 16;
+  const int ch = (lg ^ chunk_swizzle(lr)) * 8;
+  const int aoff = (wm * WM + lr) * kBK + ch;
+  const int woff = (BM + wn * WN + lr) * kBK + ch;
+  auto compute = [&](auto S) __attribute__((always_inline)) {
+    constexpr int s = decltype(S)::value;
+    bf16x8 af[TM], wf[TN];
 #pragma unroll
-    for (int ks = 0; ks < kBK / 32; ++ks) {
-      bf16x8 af[TM], wf[TN];
+    for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const bf16x8*>(&sm[s][aoff + i * 16 * kBK]);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) wf[j] = *reinterpret_cast<const bf16x8*>(&sm[s][woff + j * 16 * kBK]);
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int i = 0; i < TM; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(&As[buf][wm * WM + i * 16 + lr][ks * 32 + lk]);
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        wf[j] = *reinterpret_cast<const bf16x8*>(&Bs[buf][wn * WN + j * 16 + lr][ks * 32 + lk]);
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-          acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j], af[i], acc[j][i], 0, 0, 0);
-    }
+        acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j], af[i], acc[j][i], 0, 0, 0);
+  };
+  // one K step on stage slot J: this wave's loads of stage kt have landed (the
+  // ST-2 newer stages may still be in flight) and its LDS reads are done;
+  // after the barrier everyone's are, and the slot read in the previous step
+  // is free for stage kt+ST-1.  Past the last stage the loads repeat it into
+  // slots nobody reads again, which keeps the wait counts uniform.
+  auto step = [&](auto J, int kt) __attribute__((always_inline)) {
+    constexpr int j = decltype(J)::value;
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0((ST - 2) * IPW));
+    compiler_fence();
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+    issue(std::integral_constant<int, (j + ST - 1) % ST>{}, min(kt + ST - 1, nk - 1));
+    compute(J);
   };
 
-  // prologue: tiles 0 .. PF-1 in flight, tile 0 into LDS
-  static_for<PF>([&](auto P) __attribute__((always_inline)) {
-    if (decltype(P)::value < nk) gload(P, decltype(P)::value);
+  static_for<ST - 1>([&](auto P) __attribute__((always_inline)) { issue(P, min((int)decltype(P)::value, nk - 1)); });
+  const int nfull = nk / ST * ST;
+  for (int kt0 = 0; kt0 < nfull; kt0 += ST)
+    static_for<ST>([&](auto J) __attribute__((always_inline)) { step(J, kt0 + decltype(J)::value); });
+  static_for<ST - 1>([&](auto J) __attribute__((always_inline)) {
+    const int kt = nfull + decltype(J)::value;
+    if (kt < nk) step(J, kt);
   });
-  sstore(std::integral_constant<int, 0>{}, 0);
-  __syncthreads();
-  // steady state, unrolled by PF: register slot of tile t is t % PF, LDS
-  // buffer t % 2.  Full groups of PF tiles run branch-free (the prefetch index
-  // is clamped to the last tile, and a store after the last tile lands in the
-  // buffer nobody reads again), so the compiler's wait counts stay exact and
-  // PF tiles really are in flight; only the last partial group branches.
-  const int nfull = nk / PF * PF;
-  for (int kt0 = 0; kt0 < nfull; kt0 += PF) {
-    static_for<PF>([&](auto J) __attribute__((always_inline)) {
-      constexpr int j = decltype(J)::value;
-      const int kt = kt0 + j;
-      gload(J, min(kt + PF, nk - 1));  // slot j held tile kt, already in LDS
-      compute(kt & 1);
-      sstore(std::integral_constant<int, (j + 1) % PF>{}, (kt + 1) & 1);
-      __syncthreads();
-    });
-  }
-  static_for<PF>([&](auto J) __attribute__((always_inline)) {
-    constexpr int j = decltype(J)::value;
-    const int kt = nfull + j;
-    if (kt < nk) {
-      compute(kt & 1);
-      if (kt + 1 < nk) sstore(std::integral_constant<int, (j + 1) % PF>{}, (kt + 1) & 1);
-      __syncthreads();
-    }
-  });
+  // no load may still be writing this block's LDS when the block retires
+  __builtin_amdgcn_s_waitcnt(0);
 
   // accumulator (j,i) element r: row m = i*16 + lane%16, column n = j*16 + 4*(lane/16) + r
   if constexpr (SPLIT) {
@@ -215,6 +207,19 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
   } else if constexpr (EPI == EPI_QKV) {
     const QkvOut& qo = a.qkv;
     const int D = qo.D;
+    // per-lane constants hoisted out of the store loop: bias of the lane's
+    // columns and the q / k gains of its head dims (d = jj*16 + 4*lg + r)
+    f32x4 bias[TN], qg[4], kg[4];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bias[j] = *reinterpret_cast<const f32x4*>(a.bias + n0 + wn * WN + j * 16 + lg * 4);
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      qg[jj] = kg[jj] = f32x4{1.f, 1.f, 1.f, 1.f};
+      if (qo.qk_norm) {
+        qg[jj] = *reinterpret_cast<const f32x4*>(qo.q_g + jj * 16 + lg * 4);
+        kg[jj] = *reinterpret_cast<const f32x4*>(qo.k_g + jj * 16 + lg * 4);
+      }
+    }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       const int m = m0 + wm * WM + i * 16 + lr;
@@ -223,33 +228,25 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
       for (int hs = 0; hs < WN / 64; ++hs) {
         const int nh = n0 + wn * WN + hs * 64;  // first column of this head
         const int sec = nh / D, head = (nh % D) / 64;
-        float v[4][4];
+        f32x4 v[4];
         float ss = 0.f;
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) {
-          const int n = nh + jj * 16 + lg * 4;
-          const float4 bb = *reinterpret_cast<const float4*>(a.bias + n);
-          v[jj][0] = acc[hs * 4 + jj][i][0] + bb.x;
-          v[jj][1] = acc[hs * 4 + jj][i][1] + bb.y;
-          v[jj][2] = acc[hs * 4 + jj][i][2] + bb.z;
-          v[jj][3] = acc[hs * 4 + jj][i][3] + bb.w;
+          v[jj] = acc[hs * 4 + jj][i] + bias[hs * 4 + jj];
 #pragma unroll
           for (int r = 0; r < 4; ++r) ss += v[jj][r] * v[jj][r];
         }
         if (sec < 2) {
           ss += __shfl_xor(ss, 16, 64);
           ss += __shfl_xor(ss, 32, 64);
-          const float* gain = sec == 0 ? qo.q_g : qo.k_g;
+          const f32x4* gain = sec == 0 ? qg : kg;
           const float rs = qo.qk_norm ? rsqrtf(ss * (1.0f / 64.0f) + qo.eps) : 1.0f;
           if (m < a.M) {
             bf16* dst = (sec == 0 ? qo.q : qo.k) + (((size_t)b * qo.H + head) * qo.Tpad + t) * 64;
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
-              const int d = jj * 16 + lg * 4;
-              float4 gg = make_float4(1.f, 1.f, 1.f, 1.f);
-              if (qo.qk_norm) gg = *reinterpret_cast<const float4*>(gain + d);
-              store_bf16x4(dst + d, v[jj][0] * rs * gg.x, v[jj][1] * rs * gg.y, v[jj][2] * rs * gg.z,
-                           v[jj][3] * rs * gg.w);
+              const f32x4 o = v[jj] * rs * gain[jj];
+              store_bf16x4(dst + jj * 16 + lg * 4, o[0], o[1], o[2], o[3]);
             }
           }
         } else if (m < a.M) {
@@ -263,14 +260,38 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
       }
     }
   } else {
+    // bias (and gate) of this lane's columns once, in registers: the output
+    // may alias them as far as the compiler knows, so loads inside the store
+    // loop would be repeated and serialised behind every store
+    f32x4 bias[TN], gate[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = n0 + wn * WN + j * 16 + lg * 4;
+      bias[j] = *reinterpret_cast<const f32x4*>(a.bias + n);
+      if constexpr (EPI == EPI_GATED_RES) gate[j] = *reinterpret_cast<const f32x4*>(a.gate + n);
+    }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       const int m = m0 + wm * WM + i * 16 + lr;
       if (m >= a.M) continue;
+      if constexpr (EPI == EPI_GATED_RES) {
+        // residual stream h += gate * (acc + bias): all loads of the row first
+        f32x4* hrow = reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + (size_t)m * a.N + n0 + wn * WN + lg * 4);
+        f32x4 hv[TN];
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int n = n0 + wn * WN + j * 16 + lg * 4;
-        epi4<EPI>(a, m, n, acc[j][i][0], acc[j][i][1], acc[j][i][2], acc[j][i][3]);
+        for (int j = 0; j < TN; ++j) hv[j] = hrow[j * 4];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) hrow[j * 4] = hv[j] + gate[j] * (acc[j][i] + bias[j]);
+      } else {
+        bf16* orow = static_cast<bf16*>(a.out) + (size_t)m * a.N + n0 + wn * WN + lg * 4;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const f32x4 v = acc[j][i] + bias[j];
+          if constexpr (EPI == EPI_BIAS_GELU)
+            store_bf16x4(orow + j * 16, gelu_tanh_f(v[0]), gelu_tanh_f(v[1]), gelu_tanh_f(v[2]), gelu_tanh_f(v[3]));
+          else
+            store_bf16x4(orow + j * 16, v[0], v[1], v[2], v[3]);
+        }
       }
     }
   }
@@ -289,36 +310,36 @@ __global__ __launch_bounds__(256) void gemm_splitk_reduce_kernel(GemmArgs a, int
   epi4<EPI>(a, m, n, sum[0], sum[1], sum[2], sum[3]);
 }
 
-template <int BM, int BN, int WGM, int WGN, int PF, int ROLE>
+template <int BM, int BN, int WGM, int WGN, int ST, int ROLE>
 hipError_t launch_tile(const GemmArgs& a, int splits, hipStream_t s) {
   const int blocks = ((a.M + BM - 1) / BM) * (a.N / BN);
   constexpr int NT = WGM * WGN * 64;
   if (splits > 1) {
     dim3 grid(blocks, 1, splits);
-    gemm_bf16_kernel<BM, BN, WGM, WGN, PF, EPI_BIAS, ROLE, true><<<grid, NT, 0, s>>>(a);
+    launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, EPI_BIAS, ROLE, true>, grid, NT, 0, s, a);
     const int64_t n4 = (int64_t)a.M * a.N / 4;
     const unsigned rb = (unsigned)((n4 + 255) / 256);
     switch (a.epi) {
-      case EPI_BIAS: gemm_splitk_reduce_kernel<EPI_BIAS, ROLE><<<rb, 256, 0, s>>>(a, splits); break;
-      case EPI_BIAS_GELU: gemm_splitk_reduce_kernel<EPI_BIAS_GELU, ROLE><<<rb, 256, 0, s>>>(a, splits); break;
-      case EPI_GATED_RES: gemm_splitk_reduce_kernel<EPI_GATED_RES, ROLE><<<rb, 256, 0, s>>>(a, splits); break;
+      case EPI_BIAS: launch_k(gemm_splitk_reduce_kernel<EPI_BIAS, ROLE>, rb, 256, 0, s, a, splits); break;
+      case EPI_BIAS_GELU: launch_k(gemm_splitk_reduce_kernel<EPI_BIAS_GELU, ROLE>, rb, 256, 0, s, a, splits); break;
+      case EPI_GATED_RES: launch_k(gemm_splitk_reduce_kernel<EPI_GATED_RES, ROLE>, rb, 256, 0, s, a, splits); break;
       default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
   }
   switch (a.epi) {
     case EPI_BIAS:
-      gemm_bf16_kernel<BM, BN, WGM, WGN, PF, EPI_BIAS, ROLE, false><<<blocks, NT, 0, s>>>(a);
+      launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, EPI_BIAS, ROLE, false>, blocks, NT, 0, s, a);
       break;
     case EPI_BIAS_GELU:
-      gemm_bf16_kernel<BM, BN, WGM, WGN, PF, EPI_BIAS_GELU, ROLE, false><<<blocks, NT, 0, s>>>(a);
+      launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, EPI_BIAS_GELU, ROLE, false>, blocks, NT, 0, s, a);
       break;
     case EPI_GATED_RES:
-      gemm_bf16_kernel<BM, BN, WGM, WGN, PF, EPI_GATED_RES, ROLE, false><<<blocks, NT, 0, s>>>(a);
+      launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, EPI_GATED_RES, ROLE, false>, blocks, NT, 0, s, a);
       break;
     case EPI_QKV:
       if constexpr ((BN / WGN) % 64 == 0) {
-        gemm_bf16_kernel<BM, BN, WGM, WGN, PF, EPI_QKV, ROLE, false><<<blocks, NT, 0, s>>>(a);
+        launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, EPI_QKV, ROLE, false>, blocks, NT, 0, s, a);
       } else {
         return hipErrorInvalidValue;
       }

@@ -318,11 +318,11 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
 hipError_t launch_qkv_relayout(const RelayoutArgs& a, bool bf16_mode, hipStream_t s) {
   dim3 grid((a.T + 63) / 64, a.H, a.B);
   if (a.dh == 64) {
-    if (bf16_mode) qkv_relayout_kernel<bf16, 64><<<grid, 256, 0, s>>>(a);
-    else qkv_relayout_kernel<float, 64><<<grid, 256, 0, s>>>(a);
+    if (bf16_mode) launch_k(qkv_relayout_kernel<bf16, 64>, grid, 256, 0, s, a);
+    else launch_k(qkv_relayout_kernel<float, 64>, grid, 256, 0, s, a);
   } else if (a.dh == 32) {
-    if (bf16_mode) qkv_relayout_kernel<bf16, 32><<<grid, 256, 0, s>>>(a);
-    else qkv_relayout_kernel<float, 32><<<grid, 256, 0, s>>>(a);
+    if (bf16_mode) launch_k(qkv_relayout_kernel<bf16, 32>, grid, 256, 0, s, a);
+    else launch_k(qkv_relayout_kernel<float, 32>, grid, 256, 0, s, a);
   } else {
     return hipErrorInvalidValue;
   }
@@ -339,15 +339,15 @@ hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int pf, hipSt
   const dim3 grid((a.T + qb - 1) / qb, a.B * a.H);
   const int key = qt * 10000 + nw * 100 + pf;
   switch (key) {
-    case 10203: attn_bf16_kernel<1, 2, 3><<<grid, 128, 0, s>>>(a, scale_log2); break;
-    case 10207: attn_bf16_kernel<1, 2, 7><<<grid, 128, 0, s>>>(a, scale_log2); break;
-    case 10403: attn_bf16_kernel<1, 4, 3><<<grid, 256, 0, s>>>(a, scale_log2); break;
-    case 10407: attn_bf16_kernel<1, 4, 7><<<grid, 256, 0, s>>>(a, scale_log2); break;
-    case 10803: attn_bf16_kernel<1, 8, 3><<<grid, 512, 0, s>>>(a, scale_log2); break;
-    case 20403: attn_bf16_kernel<2, 4, 3><<<grid, 256, 0, s>>>(a, scale_log2); break;
-    case 20803: attn_bf16_kernel<2, 8, 3><<<grid, 512, 0, s>>>(a, scale_log2); break;
-    case 20805: attn_bf16_kernel<2, 8, 5><<<grid, 512, 0, s>>>(a, scale_log2); break;
-    case 40402: attn_bf16_kernel<4, 4, 2><<<grid, 256, 0, s>>>(a, scale_log2); break;
+    case 10203: launch_k(attn_bf16_kernel<1, 2, 3>, grid, 128, 0, s, a, scale_log2); break;
+    case 10207: launch_k(attn_bf16_kernel<1, 2, 7>, grid, 128, 0, s, a, scale_log2); break;
+    case 10403: launch_k(attn_bf16_kernel<1, 4, 3>, grid, 256, 0, s, a, scale_log2); break;
+    case 10407: launch_k(attn_bf16_kernel<1, 4, 7>, grid, 256, 0, s, a, scale_log2); break;
+    case 10803: launch_k(attn_bf16_kernel<1, 8, 3>, grid, 512, 0, s, a, scale_log2); break;
+    case 20403: launch_k(attn_bf16_kernel<2, 4, 3>, grid, 256, 0, s, a, scale_log2); break;
+    case 20803: launch_k(attn_bf16_kernel<2, 8, 3>, grid, 512, 0, s, a, scale_log2); break;
+    case 20805: launch_k(attn_bf16_kernel<2, 8, 5>, grid, 512, 0, s, a, scale_log2); break;
+    case 40402: launch_k(attn_bf16_kernel<4, 4, 2>, grid, 256, 0, s, a, scale_log2); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -362,8 +362,8 @@ hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s) {
     return launch_attention_cfg(a, 1, 4, 3, s);
   }
   dim3 grid((a.T + 63) / 64, a.B * a.H);
-  if (a.dh == 64) attn_f32_kernel<64><<<grid, 64, 0, s>>>(a);
-  else if (a.dh == 32) attn_f32_kernel<32><<<grid, 64, 0, s>>>(a);
+  if (a.dh == 64) launch_k(attn_f32_kernel<64>, grid, 64, 0, s, a);
+  else if (a.dh == 32) launch_k(attn_f32_kernel<32>, grid, 64, 0, s, a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

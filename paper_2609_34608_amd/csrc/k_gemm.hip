@@ -11,30 +11,27 @@ using gemm::launch_tile;
 
 // ---------------------------------------------------------------- configs
 struct TileCfg {
-  int bm, bn, wgm, wgn, pf;
+  int bm, bn, wgm, wgn, st;
 };
-// index: tile rows x cols, waves (rows x cols), K tiles in flight
+// index: tile rows x cols, waves (rows x cols), LDS stages of 32 K
 constexpr TileCfg kCfgs[] = {
     {64, 64, 2, 2, 4},    // 0
     {64, 128, 2, 2, 4},   // 1
     {128, 64, 2, 2, 4},   // 2
-    {128, 128, 2, 2, 3},  // 3
-    {128, 128, 2, 4, 4},  // 4
-    {256, 128, 4, 2, 3},  // 5
-    {128, 256, 2, 4, 3},  // 6
-    {256, 256, 4, 4, 1},  // 7
-    {256, 128, 2, 2, 2},  // 8
-    {128, 256, 2, 2, 2},  // 9
-    {256, 128, 4, 2, 4},  // 10
-    {256, 256, 2, 2, 1},  // 11
-    {128, 256, 2, 4, 4},  // 12
+    {128, 128, 2, 2, 4},  // 3
+    {256, 256, 2, 4, 4},  // 4
+    {256, 256, 4, 2, 4},  // 5
+    {256, 128, 2, 4, 4},  // 6
+    {128, 256, 2, 4, 4},  // 7
+    {128, 128, 2, 4, 4},  // 8
+    {64, 256, 1, 4, 4},   // 9
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
 template <int C, int ROLE>
 hipError_t launch_c(const GemmArgs& a, int splits, hipStream_t s) {
   constexpr TileCfg t = kCfgs[C];
-  return launch_tile<t.bm, t.bn, t.wgm, t.wgn, t.pf, ROLE>(a, splits, s);
+  return launch_tile<t.bm, t.bn, t.wgm, t.wgn, t.st, ROLE>(a, splits, s);
 }
 
 template <int ROLE>
@@ -49,10 +46,7 @@ hipError_t launch_role(const GemmArgs& a, int cfg, int splits, hipStream_t s) {
     case 6: return launch_c<6, ROLE>(a, splits, s);
     case 7: return launch_c<7, ROLE>(a, splits, s);
     case 8: return launch_c<8, ROLE>(a, splits, s);
-    case 9: return launch_c<9, ROLE>(a, splits, s);
-    case 10: return launch_c<10, ROLE>(a, splits, s);
-    case 12: return launch_c<12, ROLE>(a, splits, s);
-    default: return launch_c<11, ROLE>(a, splits, s);
+    default: return launch_c<9, ROLE>(a, splits, s);
   }
 }
 
@@ -126,15 +120,12 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 int gemm_num_configs() { return kNumCfgs; }
 
 GemmPlan plan_gemm(int M, int N, int K, int epi) {
-  // Chosen from a sweep of every tile configuration at the workload shapes:
-  // 256x256 tiles with 16 waves (64x64 each, one K tile in flight, four waves
-  // per SIMD) once M gives enough tile rows; below that 64x64 tiles (64x128
-  // for the QKV epilogue, which needs whole heads per wave).  With K tiles in
-  // flight the small-M shapes no longer gain from splitting K; a split is kept
-  // for grids under half a block per CU.
+  // 256x256 tiles with 8 waves (128x64 each) once M gives enough tile rows;
+  // below that 64x64 tiles (64x128 for the QKV epilogue, which needs whole
+  // heads per wave); a K split only for grids under half a block per CU.
   GemmPlan p{0, 1};
   if (M >= 2048 && N % 256 == 0) {
-    p.cfg = 7;
+    p.cfg = 4;
     return p;
   }
   if (epi == EPI_QKV) {
@@ -176,9 +167,9 @@ hipError_t launch_gemm(const GemmArgs& a, bool bf16_mode, hipStream_t s) {
   if (a.K % kFK || a.epi == EPI_QKV) return hipErrorInvalidValue;
   dim3 grid((a.N + kFT - 1) / kFT, (a.M + kFT - 1) / kFT);
   switch (a.epi) {
-    case EPI_BIAS: gemm_f32_kernel<EPI_BIAS><<<grid, 256, 0, s>>>(a); break;
-    case EPI_BIAS_GELU: gemm_f32_kernel<EPI_BIAS_GELU><<<grid, 256, 0, s>>>(a); break;
-    case EPI_GATED_RES: gemm_f32_kernel<EPI_GATED_RES><<<grid, 256, 0, s>>>(a); break;
+    case EPI_BIAS: launch_k(gemm_f32_kernel<EPI_BIAS>, grid, 256, 0, s, a); break;
+    case EPI_BIAS_GELU: launch_k(gemm_f32_kernel<EPI_BIAS_GELU>, grid, 256, 0, s, a); break;
+    case EPI_GATED_RES: launch_k(gemm_f32_kernel<EPI_GATED_RES>, grid, 256, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

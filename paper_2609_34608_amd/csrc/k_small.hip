@@ -497,8 +497,8 @@ hipError_t launch_timestep_mlp(float sigma, const float* w1, const float* b1, co
                                float* a1, float* silu_c, int D, hipStream_t s) {
   if (D > 2048) return hipErrorInvalidValue;
   const int grid = (D + kSgN - 1) / kSgN;
-  small_gemv_silu_kernel<true><<<grid, kSgN * kSgK, 0, s>>>(sigma, nullptr, w1, b1, a1, kTimeDim, D);
-  small_gemv_silu_kernel<false><<<grid, kSgN * kSgK, 0, s>>>(0.f, a1, w2, b2, silu_c, D, D);
+  launch_k(small_gemv_silu_kernel<true>, grid, kSgN * kSgK, 0, s, sigma, nullptr, w1, b1, a1, kTimeDim, D);
+  launch_k(small_gemv_silu_kernel<false>, grid, kSgN * kSgK, 0, s, 0.f, a1, w2, b2, silu_c, D, D);
   return hipGetLastError();
 }
 
@@ -508,16 +508,16 @@ hipError_t launch_gemv(const float* x, const void* W, bool w_bf16, const float* 
   const int nchunk = (K + kGemvKc - 1) / kGemvKc;
   dim3 grid((N / kGemvVec + 255) / 256, nchunk);
   if (w_bf16)
-    gemv_partial_kernel<bf16><<<grid, 256, 0, s>>>(x, (const bf16*)W, partial, K, N, in_act);
+    launch_k(gemv_partial_kernel<bf16>, grid, 256, 0, s, x, (const bf16*)W, partial, K, N, in_act);
   else
-    gemv_partial_kernel<float><<<grid, 256, 0, s>>>(x, (const float*)W, partial, K, N, in_act);
-  gemv_reduce_kernel<<<(N + 255) / 256, 256, 0, s>>>(partial, b, y, nchunk, N, out_act);
+    launch_k(gemv_partial_kernel<float>, grid, 256, 0, s, x, (const float*)W, partial, K, N, in_act);
+  launch_k(gemv_reduce_kernel, (N + 255) / 256, 256, 0, s, partial, b, y, nchunk, N, out_act);
   return hipGetLastError();
 }
 
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
   if (a.Cv > 64 || a.A > 64 || a.Co > 64) return hipErrorInvalidValue;
-  embed_kernel<<<a.B * a.T, 256, 0, s>>>(a);
+  launch_k(embed_kernel, a.B * a.T, 256, 0, s, a);
   return hipGetLastError();
 }
 
@@ -527,11 +527,11 @@ hipError_t launch_ln_modulate(const float* h, const float* shift, const float* s
   const int wpb = 4;
   dim3 grid((rows + wpb - 1) / wpb);
   if (bf16_out && D % 256 == 0)
-    ln_modulate_v4_kernel<<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (bf16*)u, rows, D, eps, skip);
+    launch_k(ln_modulate_v4_kernel, grid, wpb * kWave, 0, s, h, shift, scale, (bf16*)u, rows, D, eps, skip);
   else if (bf16_out)
-    ln_modulate_kernel<bf16><<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (bf16*)u, rows, D, eps, skip);
+    launch_k(ln_modulate_kernel<bf16>, grid, wpb * kWave, 0, s, h, shift, scale, (bf16*)u, rows, D, eps, skip);
   else
-    ln_modulate_kernel<float><<<grid, wpb * kWave, 0, s>>>(h, shift, scale, (float*)u, rows, D, eps, skip);
+    launch_k(ln_modulate_kernel<float>, grid, wpb * kWave, 0, s, h, shift, scale, (float*)u, rows, D, eps, skip);
   return hipGetLastError();
 }
 
@@ -540,7 +540,7 @@ hipError_t launch_final(const FinalArgs& a, hipStream_t s) {
   const int rows = a.B * (a.Nv + a.Na);
   const int per_block = kFinalWaves * 4;
   const size_t lds = (size_t)per_block * a.D * sizeof(float);
-  final_kernel<<<(rows + per_block - 1) / per_block, kFinalWaves * 64, lds, s>>>(a);
+  launch_k(final_kernel, (rows + per_block - 1) / per_block, kFinalWaves * 64, lds, s, a);
   return hipGetLastError();
 }
 
@@ -548,48 +548,48 @@ hipError_t launch_rr_gate(const RRGateArgs& a, hipStream_t s) {
   const int rows = a.B * a.T;
   if (a.D % 4) return hipErrorInvalidValue;
   const int wpb = 4;
-  rr_row_sums_kernel<<<(rows + wpb - 1) / wpb, wpb * kWave, 0, s>>>(a.hs, a.hq, a.pa, a.row_sums, rows, a.D);
-  rr_finish_kernel<<<a.B * 2, 1024, 0, s>>>(a);
+  launch_k(rr_row_sums_kernel, (rows + wpb - 1) / wpb, wpb * kWave, 0, s, a.hs, a.hq, a.pa, a.row_sums, rows, a.D);
+  launch_k(rr_finish_kernel, a.B * 2, 1024, 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_rr_inject(float* h, const float* Ra, const double* result, int B, int T, int D,
                             int Nv, int Na, hipStream_t s, const int* flag) {
   const int64_t n4 = (int64_t)B * T * D / 4;
-  rr_inject_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(h, Ra, result, B * T, T, D, Nv, Na, flag);
+  launch_k(rr_inject_kernel, (unsigned)((n4 + 255) / 256), 256, 0, s, h, Ra, result, B * T, T, D, Nv, Na, flag);
   return hipGetLastError();
 }
 
 hipError_t launch_rr_pre_middle(const float* h, float* hq, float* pa, int64_t n, hipStream_t s,
                                 const int* flag) {
   const int64_t n4 = n / 4;
-  rr_pre_middle_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(h, hq, pa, n4, flag);
+  launch_k(rr_pre_middle_kernel, (unsigned)((n4 + 255) / 256), 256, 0, s, h, hq, pa, n4, flag);
   return hipGetLastError();
 }
 
 hipError_t launch_rr_refresh(const float* h, const float* hq, float* Ra, int64_t n, hipStream_t s,
                              const int* flag) {
   const int64_t n4 = n / 4;
-  rr_refresh_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(h, hq, Ra, n4, flag);
+  launch_k(rr_refresh_kernel, (unsigned)((n4 + 255) / 256), 256, 0, s, h, hq, Ra, n4, flag);
   return hipGetLastError();
 }
 
 hipError_t launch_rr_decide(const double* result, int B, int force_accept, int* flag, double* hist_stats,
                             int* hist_flag, hipStream_t s) {
-  rr_decide_kernel<<<1, 64, 0, s>>>(result, B, force_accept, flag, hist_stats, hist_flag);
+  launch_k(rr_decide_kernel, 1, 64, 0, s, result, B, force_accept, flag, hist_stats, hist_flag);
   return hipGetLastError();
 }
 
 hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  copy_f32_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(src, dst, n);
+  launch_k(copy_f32_kernel, (unsigned)((n + 255) / 256), 256, 0, s, src, dst, n);
   return hipGetLastError();
 }
 
 hipError_t launch_remap(const RemapArgs& a, hipStream_t s) {
-  remap_rms_kernel<<<a.B * 2, 256, 0, s>>>(a);
+  launch_k(remap_rms_kernel, a.B * 2, 256, 0, s, a);
   const int64_t n = (int64_t)a.B * (a.Nv * a.Cv + a.Na * a.A);
-  remap_apply_kernel<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(a);
+  launch_k(remap_apply_kernel, (unsigned)((n + 255) / 256), 256, 0, s, a);
   return hipGetLastError();
 }
 
@@ -604,7 +604,7 @@ hipError_t launch_or_sums(int n_comp, const float* const* u_hat, const float* co
     a.inv_delta[m] = 1.0 / delta[m];
   }
   a.sums = sums;
-  or_sums_kernel<<<n_comp, 256, 0, s>>>(a);
+  launch_k(or_sums_kernel, n_comp, 256, 0, s, a);
   return hipGetLastError();
 }
 

@@ -283,15 +283,16 @@ struct ProfScope {
     ProfSlot& p = h->prof[kc];
     if (p.on && p.used < p.max && !h->capturing) {
       on = true;
-      hipEventRecord(p.ev[2 * p.used], h->stream);
+      launch_timing() = LaunchTiming{p.ev[2 * p.used], p.ev[2 * p.used + 1], false};
       p.work[p.used] = work;
     }
   }
   ~ProfScope() {
     if (on) {
       ProfSlot& p = h->prof[kc];
-      hipEventRecord(p.ev[2 * p.used + 1], h->stream);
-      ++p.used;
+      // a scope whose kernels were all skipped on the host has nothing to time
+      if (launch_timing().started) ++p.used;
+      launch_timing() = LaunchTiming{};
     }
   }
 };

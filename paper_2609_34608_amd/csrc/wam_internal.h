@@ -1,6 +1,7 @@
 // Internal declarations shared by the libwam translation units (gfx950 only).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -17,6 +18,33 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
+
+// ---------------------------------------------------------------- launches
+// Per-class kernel timing.  While a timing scope is armed (start / stop
+// events set), launches go through hipExtLaunchKernel, which stamps the start
+// event with the begin of the scope's first dispatch and the stop event with
+// the end of each dispatch: the event pair spans exactly the scope's kernels,
+// with no event-record packets in between.  Unarmed, a launch is a plain one.
+struct LaunchTiming {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+  bool started = false;  // the start event has been attached to a dispatch
+};
+inline LaunchTiming& launch_timing() {
+  static thread_local LaunchTiming t;
+  return t;
+}
+template <typename... KArgs, typename... Args>
+inline void launch_k(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t lds, hipStream_t s, Args... args) {
+  LaunchTiming& t = launch_timing();
+  if (t.stop) {
+    hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, s, t.started ? nullptr : t.start, t.stop, 0u,
+                          static_cast<KArgs>(args)...);
+    t.started = true;
+  } else {
+    kernel<<<grid, block, lds, s>>>(static_cast<KArgs>(args)...);
+  }
+}
 
 // compile-time loop: f(std::integral_constant<int, 0>) ... f(<N-1>); keeps
 // register-array indices static after inlining
