@@ -219,6 +219,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
         qg[jj] = *reinterpret_cast<const f32x4*>(qo.q_g + jj * 16 + lg * 4);
         kg[jj] = *reinterpret_cast<const f32x4*>(qo.k_g + jj * 16 + lg * 4);
       }
+      qg[jj] *= kQLog2Scale;  // attention scores come out in log2 units
     }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
@@ -250,7 +251,8 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
             }
           }
         } else if (m < a.M) {
-          bf16* dst = qo.vt + ((size_t)b * qo.H + head) * 64 * qo.Tpad + t;
+          // V^T row d holds the tokens of each 64-key block in vt_key_pos order
+          bf16* dst = qo.vt + ((size_t)b * qo.H + head) * 64 * qo.Tpad + (t & ~63) + vt_key_pos(t & 63);
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj)
 #pragma unroll

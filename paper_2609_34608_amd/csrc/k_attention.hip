@@ -10,11 +10,19 @@
 // v_mfma_f32_16x16x32_bf16 so that a lane's accumulators all belong to one
 // query column: the online-softmax rescale of O^T = V^T P^T is lane-local and
 // the running max needs only two cross-lane steps.  P^T feeds the second MFMA
-// straight from registers; the key order inside the 32-key contraction is
-// permuted consistently on both operands (a contraction is order-free), so V^T
-// is read from LDS as two 8-byte runs per lane.  K and V^T tiles of 64 keys are
-// double-buffered in LDS and prefetched through registers.  Softmax runs in
-// fp32 with exp2 and a log2(e)/sqrt(dh) pre-scale.
+// straight from registers; the key order inside the 32-key contraction is the
+// one the score accumulators hold, and the QKV epilogue stores V^T with its
+// keys permuted to match (vt_key_pos), so each V^T operand is one 16-byte LDS
+// read.  K and V^T tiles of 64 keys (128-byte rows, 16-byte chunks XOR-swizzled
+// by row & 7: conflict-free ds_read_b128) go through ST LDS stages filled by
+// global_load_lds_dwordx4, ST-1 in flight.  Softmax runs in fp32 with exp2: q
+// arrives pre-scaled by log2(e)/sqrt(dh) (QKV epilogue), and the score
+// accumulators start at -m, the query's running max, so a score comes out of
+// the MFMA as its exp2 argument.  m only moves (and O is only rescaled) when
+// a tile raises a query's max by more than 8, which keeps every p <= 2^8 and
+// leaves the normalised result unchanged; the first tile always sets it.  The
+// softmax denominator is one more MFMA per 32 keys (a ones operand against
+// P^T), summing exactly the bf16 P that multiplies V.
 #include <math.h>
 
 #include "wam_internal.h"
@@ -69,17 +77,26 @@ __global__ __launch_bounds__(256) void qkv_relayout_kernel(RelayoutArgs a) {
 
 // ------------------------------------------------------------- bf16 flash attention
 constexpr int kDh = 64;
-constexpr int kKB = 64;           // keys per tile
-constexpr int kKL = kDh + 8;      // LDS row (K tile): 64 dh + pad
-constexpr int kVL = kKB + 8;      // LDS row (V^T tile): 64 keys + pad
+constexpr int kKB = 64;  // keys per tile
 
-template <int QT, int NW, int PF>
-__global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float scale_log2) {
-  if (a.skip && *a.skip) return;
-  constexpr int NT = NW * 64;
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void global_void;
+
+// s_waitcnt immediate (gfx9 layout): at most n vector-memory operations and no
+// LDS operation outstanding
+constexpr int waitcnt_vm_lgkm0(int n) { return (n & 0xf) | ((n >> 4) << 14) | (0x7 << 4); }
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
+
+template <int QT, int NW, int ST>
+__global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   constexpr int QB = NW * QT * 16;  // queries per block
-  __shared__ __attribute__((aligned(16))) bf16 Ks[2][kKB][kKL];
-  __shared__ __attribute__((aligned(16))) bf16 Vs[2][kDh][kVL];
+  constexpr int NI = 16;            // 1 KiB load instructions per stage: K rows 0-63, V^T rows 64-127
+  constexpr int IPW = NI / NW;
+  static_assert(IPW >= 1 && IPW * NW == NI, "stage load split");
+  static_assert(ST >= 2 && (ST - 2) * IPW < 64, "stage count");
+  if (a.skip && *a.skip) return;
+  // stage: 128 rows of 64 bf16 (128 bytes); chunk c of row r stored at c ^ (r & 7)
+  __shared__ __attribute__((aligned(1024))) bf16 sm[ST][128 * kDh];
 
   const int bh = blockIdx.y;
   const int b = bh / a.H, h = bh % a.H;
@@ -103,51 +120,55 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
     }
 
   f32x4 o[4][QT];  // O^T tiles: dh tile x query tile
-#pragma unroll
-  for (int d = 0; d < 4; ++d)
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) o[d][qt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float mrun[QT], lrun[QT];
+  f32x4 l[QT];     // softmax denominators (all four elements equal)
+  float mrun[QT];  // running max, log2 units; 0 until the first tile sets it
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
-    mrun[qt] = -INFINITY;
-    lrun[qt] = 0.f;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) o[d][qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    l[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    mrun[qt] = 0.f;
   }
-
-  // K and V^T tiles of 64 keys: 512 chunks of 16 B each, CH per thread;
-  // register slots hold the next PF tiles (slot of tile t is t % PF)
-  constexpr int CH = 512 / NT;
-  static_assert(CH >= 1 && CH * NT == 512, "tile load split");
-  u32x4 rk[PF][CH], rv[PF][CH];
-  auto gload = [&](auto S, int k0) __attribute__((always_inline)) {
-    constexpr int slot = decltype(S)::value;
+  bf16x8 ones;
 #pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
-      rk[slot][i] = *reinterpret_cast<const u32x4*>(Kg + (size_t)(k0 + row) * kDh + col);
-      rv[slot][i] = *reinterpret_cast<const u32x4*>(Vg + (size_t)row * a.Tpad + k0 + col);
+  for (int i = 0; i < 8; ++i) ones[i] = static_cast<bf16>(1.0f);
+
+  // Load instruction j of this wave fills stage rows 8*i .. 8*i+7 with
+  // i = wid + NW*j; lane l writes chunk l%8 of row l/8, i.e. global chunk
+  // (l%8) ^ (row & 7).  Rows 0-63 are keys (K rows), rows 64-127 are dh rows
+  // of V^T; the next key tile is 64 K rows or 64 V^T columns further on.
+  const bf16* src[IPW];
+#pragma unroll
+  for (int j = 0; j < IPW; ++j) {
+    const int row = 8 * (wid + NW * j) + lane / 8;
+    const int col = ((lane % 8) ^ (row & 7)) * 8;
+    src[j] = j < IPW / 2 ? Kg + (size_t)row * kDh + col : Vg + (size_t)(row - 64) * a.Tpad + col;
+  }
+  auto issue = [&](auto S, int kb) __attribute__((always_inline)) {
+    constexpr int s = decltype(S)::value;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      // instructions 0-7 of a stage (j < IPW/2 for every wave) carry K rows
+      const size_t step = j < IPW / 2 ? (size_t)kKB * kDh : (size_t)kKB;
+      __builtin_amdgcn_global_load_lds((const global_void*)(src[j] + kb * step),
+                                       (lds_void*)(&sm[s][(wid + NW * j) * 512]), 16, 0, 0);
     }
   };
-  auto sstore = [&](auto S, int buf) __attribute__((always_inline)) {
-    constexpr int slot = decltype(S)::value;
-#pragma unroll
-    for (int i = 0; i < CH; ++i) {
-      const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
-      *reinterpret_cast<u32x4*>(&Ks[buf][row][col]) = rk[slot][i];
-      *reinterpret_cast<u32x4*>(&Vs[buf][row][col]) = rv[slot][i];
-    }
-  };
 
-  auto block = [&](int buf, int k0, auto MASK) __attribute__((always_inline)) {
-    // S^T tiles [key tile kt][query tile qt]
+  const int sw = lr & 7;  // swizzle of every row this lane reads (tile rows are multiples of 16)
+  auto block = [&](auto S, int k0, auto MASK, bool first) __attribute__((always_inline)) {
+    const bf16* st = sm[decltype(S)::value];
+    // S^T - m tiles [key tile kt][query tile qt]: the accumulators start at -m
     f32x4 s[4][QT];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
-      const bf16x8 k0f = *reinterpret_cast<const bf16x8*>(&Ks[buf][kt * 16 + lr][g * 8]);
-      const bf16x8 k1f = *reinterpret_cast<const bf16x8*>(&Ks[buf][kt * 16 + lr][32 + g * 8]);
+      const bf16* krow = st + (kt * 16 + lr) * kDh;
+      const bf16x8 k0f = *reinterpret_cast<const bf16x8*>(krow + ((g ^ sw) * 8));
+      const bf16x8 k1f = *reinterpret_cast<const bf16x8*>(krow + (((g + 4) ^ sw) * 8));
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt) {
-        f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        const float nm = -mrun[qt];
+        f32x4 z = {nm, nm, nm, nm};
         z = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0f, qf[qt][0], z, 0, 0, 0);
         s[kt][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1f, qf[qt][1], z, 0, 0, 0);
       }
@@ -175,21 +196,19 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
         for (int r = 0; r < 4; ++r) mx = fmaxf(mx, s[kt][qt][r]);
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mnew = fmaxf(mrun[qt], mx * scale_log2);
-      const float corr = __builtin_amdgcn_exp2f(mrun[qt] - mnew);
-      mrun[qt] = mnew;
-      float ls = 0.f;
-      float p[4][4];
+      // move m when this tile raises some query's max by more than 8 (the
+      // branch is wave-uniform), and always on the first tile
+      if (first || __builtin_amdgcn_ballot_w64(mx > 8.0f) != 0) {
+        const float delta = first ? mx : fmaxf(mx, 0.f);
+        // first tile: O and l are still zero, any finite factor keeps them so
+        const float corr = __builtin_amdgcn_exp2f(fminf(-delta, 0.f));
+        mrun[qt] += delta;
+        l[qt] *= corr;
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
+        for (int d = 0; d < 4; ++d) o[d][qt] *= corr;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          p[kt][r] = __builtin_amdgcn_exp2f(s[kt][qt][r] * scale_log2 - mnew);
-          ls += p[kt][r];
-        }
-      lrun[qt] = lrun[qt] * corr + ls;
-#pragma unroll
-      for (int d = 0; d < 4; ++d) o[d][qt] *= corr;
+        for (int kt = 0; kt < 4; ++kt) s[kt][qt] -= delta;
+      }
       // B operand of O^T += V^T P^T for key chunk c: slots 0-3 = key tile 2c,
       // slots 4-7 = key tile 2c+1 (keys 4g+r within each)
 #pragma unroll
@@ -197,21 +216,25 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
         bf16x8 v;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          v[r] = static_cast<bf16>(p[2 * c][r]);
-          v[4 + r] = static_cast<bf16>(p[2 * c + 1][r]);
+          v[r] = static_cast<bf16>(__builtin_amdgcn_exp2f(s[2 * c][qt][r]));
+          v[4 + r] = static_cast<bf16>(__builtin_amdgcn_exp2f(s[2 * c + 1][qt][r]));
         }
         pf[c][qt] = v;
       }
     }
-    // O^T[dh][q] += V^T[dh][keys] P^T[keys][q]; A slots follow the same key permutation
+    // O^T[dh][q] += V^T[dh][keys] P^T[keys][q]: with the stored key order the
+    // eight keys of slot (c, g) are chunk 4c + g of the V^T row; the ones
+    // operand adds the column sums of P^T into l
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) l[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[c][qt], l[qt], 0, 0, 0);
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
+      const bf16* vrow = st + (64 + d * 16 + lr) * kDh;
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const bf16* vrow = &Vs[buf][d * 16 + lr][c * 32 + g * 4];
-        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
-        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 16);
-        const bf16x8 vf = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vrow + (((4 * c + g) ^ sw) * 8));
 #pragma unroll
         for (int qt = 0; qt < QT; ++qt)
           o[d][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[c][qt], o[d][qt], 0, 0, 0);
@@ -219,49 +242,41 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a, float sc
     }
   };
 
+  // one key tile on stage slot J: this wave's loads of tile kb have landed and
+  // its LDS reads are done; after the barrier everyone's are, and the slot of
+  // the previous tile takes tile kb+ST-1 (past the end the last tile again,
+  // into slots nobody reads, which keeps the wait counts uniform)
   const int nkb = a.Tpad / kKB;
-  static_for<PF>([&](auto P) __attribute__((always_inline)) {
-    if (decltype(P)::value < nkb) gload(P, decltype(P)::value * kKB);
-  });
-  sstore(std::integral_constant<int, 0>{}, 0);
-  __syncthreads();
-  // Full groups of PF tiles run branch-free (prefetch index clamped to the
-  // last tile; a store after the last tile goes to a buffer nobody reads
-  // again) so that PF tiles stay in flight.  The last tile is kept out of the
-  // groups: it runs last, with the key mask.
+  auto step = [&](auto J, int kb, auto MASK) __attribute__((always_inline)) {
+    constexpr int j = decltype(J)::value;
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0((ST - 2) * IPW));
+    compiler_fence();
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+    issue(std::integral_constant<int, (j + ST - 1) % ST>{}, min(kb + ST - 1, nkb - 1));
+    block(J, kb * kKB, MASK, kb == 0);
+  };
   const std::integral_constant<bool, false> nomask{};
   const std::integral_constant<bool, true> withmask{};
+  static_for<ST - 1>([&](auto P) __attribute__((always_inline)) { issue(P, min((int)decltype(P)::value, nkb - 1)); });
+  // tiles 0 .. nkb-2 carry no padded keys; the last one runs with the mask
   const int nbody = nkb - 1;
-  const int nfull = nbody / PF * PF;
-  for (int kb0 = 0; kb0 < nfull; kb0 += PF) {
-    static_for<PF>([&](auto J) __attribute__((always_inline)) {
-      constexpr int j = decltype(J)::value;
-      const int kb = kb0 + j;
-      gload(J, min(kb + PF, nkb - 1) * kKB);  // slot j held tile kb, already in LDS
-      block(kb & 1, kb * kKB, nomask);
-      sstore(std::integral_constant<int, (j + 1) % PF>{}, (kb + 1) & 1);
-      __syncthreads();
-    });
-  }
-  static_for<PF>([&](auto J) __attribute__((always_inline)) {
-    constexpr int j = decltype(J)::value;
-    const int kb = nfull + j;
-    if (kb < nbody) {
-      block(kb & 1, kb * kKB, nomask);
-      sstore(std::integral_constant<int, (j + 1) % PF>{}, (kb + 1) & 1);
-      __syncthreads();
-    }
+  const int nfull = nbody / ST * ST;
+  for (int kb0 = 0; kb0 < nfull; kb0 += ST)
+    static_for<ST>([&](auto J) __attribute__((always_inline)) { step(J, kb0 + decltype(J)::value, nomask); });
+  static_for<ST>([&](auto J) __attribute__((always_inline)) {
+    const int kb = nfull + decltype(J)::value;
+    if (kb < nbody) step(J, kb, nomask);
+    else if (kb == nbody) step(J, kb, withmask);
   });
-  block(nbody & 1, nbody * kKB, withmask);
+  // no load may still be writing this block's LDS when the block retires
+  __builtin_amdgcn_s_waitcnt(0);
 
   // normalise and store O[b*T + q][h*64 + dh]; lane holds dh = d*16 + 4g + r of query lr
   bf16* out = static_cast<bf16*>(a.out);
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
-    float l = lrun[qt];
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
-    const float inv = 1.0f / l;
+    const float inv = 1.0f / l[qt][0];
     const int q = q0 + qt * 16 + lr;
     if (q >= a.T) continue;
     bf16* orow = out + ((size_t)b * a.T + q) * a.D + h * kDh;
@@ -330,24 +345,23 @@ hipError_t launch_qkv_relayout(const RelayoutArgs& a, bool bf16_mode, hipStream_
 }
 
 // grid for qt query tiles per wave and nw waves per block
-// (qt, nw, pf): query tiles of 16 per wave, waves per block, K/V tiles in
-// flight.  Only the instantiated combinations are accepted.
-hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int pf, hipStream_t s) {
-  if (a.dh != kDh || a.Tpad % kKB) return hipErrorInvalidValue;
-  const float scale_log2 = 1.4426950408889634f / sqrtf((float)a.dh);
+// (qt, nw, st): query tiles of 16 per wave, waves per block, LDS stages of
+// one 64-key K / V^T tile.  Only the instantiated combinations are accepted.
+hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int st, hipStream_t s) {
+  // every key tile but the last is fully inside [0, T), the last holds >= 1 key
+  if (a.dh != kDh || a.T <= 0 || a.Tpad % kKB || a.T > a.Tpad || a.T <= a.Tpad - kKB) return hipErrorInvalidValue;
   const int qb = qt * nw * 16;
   const dim3 grid((a.T + qb - 1) / qb, a.B * a.H);
-  const int key = qt * 10000 + nw * 100 + pf;
+  const int key = qt * 10000 + nw * 100 + st;
   switch (key) {
-    case 10203: launch_k(attn_bf16_kernel<1, 2, 3>, grid, 128, 0, s, a, scale_log2); break;
-    case 10207: launch_k(attn_bf16_kernel<1, 2, 7>, grid, 128, 0, s, a, scale_log2); break;
-    case 10403: launch_k(attn_bf16_kernel<1, 4, 3>, grid, 256, 0, s, a, scale_log2); break;
-    case 10407: launch_k(attn_bf16_kernel<1, 4, 7>, grid, 256, 0, s, a, scale_log2); break;
-    case 10803: launch_k(attn_bf16_kernel<1, 8, 3>, grid, 512, 0, s, a, scale_log2); break;
-    case 20403: launch_k(attn_bf16_kernel<2, 4, 3>, grid, 256, 0, s, a, scale_log2); break;
-    case 20803: launch_k(attn_bf16_kernel<2, 8, 3>, grid, 512, 0, s, a, scale_log2); break;
-    case 20805: launch_k(attn_bf16_kernel<2, 8, 5>, grid, 512, 0, s, a, scale_log2); break;
-    case 40402: launch_k(attn_bf16_kernel<4, 4, 2>, grid, 256, 0, s, a, scale_log2); break;
+    case 10404: launch_k(attn_bf16_kernel<1, 4, 4>, grid, 256, 0, s, a); break;
+    case 20404: launch_k(attn_bf16_kernel<2, 4, 4>, grid, 256, 0, s, a); break;
+    case 40403: launch_k(attn_bf16_kernel<4, 4, 3>, grid, 256, 0, s, a); break;
+    case 10804: launch_k(attn_bf16_kernel<1, 8, 4>, grid, 512, 0, s, a); break;
+    case 20804: launch_k(attn_bf16_kernel<2, 8, 4>, grid, 512, 0, s, a); break;
+    case 20803: launch_k(attn_bf16_kernel<2, 8, 3>, grid, 512, 0, s, a); break;
+    case 40402: launch_k(attn_bf16_kernel<4, 4, 2>, grid, 256, 0, s, a); break;
+    case 20402: launch_k(attn_bf16_kernel<2, 4, 2>, grid, 256, 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -355,11 +369,11 @@ hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int pf, hipSt
 
 hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s) {
   if (bf16_mode) {
-    // 8 waves x 32 queries with 5 K/V tiles in flight when that still fills
-    // the chip, else 4 waves x 16 queries
+    // 4 waves x 32 queries (two K/V stages) when that fills the chip, else
+    // 4 waves x 16 queries
     const long blocks = (long)((a.T + 255) / 256) * a.B * a.H;
-    if (blocks >= 256) return launch_attention_cfg(a, 2, 8, 5, s);
-    return launch_attention_cfg(a, 1, 4, 3, s);
+    if (blocks >= 256) return launch_attention_cfg(a, 2, 4, 2, s);
+    return launch_attention_cfg(a, 1, 4, 4, s);
   }
   dim3 grid((a.T + 63) / 64, a.B * a.H);
   if (a.dh == 64) launch_k(attn_f32_kernel<64>, grid, 64, 0, s, a);

@@ -57,6 +57,18 @@ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
+// The bf16 QKV epilogue stores q pre-multiplied by log2(e) / sqrt(64), so the
+// bf16 attention kernel's scores are already the exponents of exp2.
+constexpr float kQLog2Scale = 0.18033688011112042f;  // log2(e) / 8
+
+// Key order inside each 64-key block of the stored V^T rows (bf16 path): key
+// 32c + 16h + 4g + r sits at 32c + 8g + 4h + r, so that the eight keys one
+// lane feeds to a P.V MFMA (rows 4g..4g+3 of two adjacent 16-key score tiles)
+// are adjacent in LDS and load as one 16-byte read.
+__host__ __device__ constexpr int vt_key_pos(int k) {
+  return (k & 32) | ((k & 12) << 1) | ((k & 16) >> 2) | (k & 3);
+}
+
 // ---------------------------------------------------------------- helpers
 __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ float to_f32(bf16 x) { return static_cast<float>(x); }
@@ -144,7 +156,7 @@ struct AttnArgs {
 };
 hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s);
 // bf16 kernel with qt query tiles of 16 per wave and nw waves per block
-hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int pf, hipStream_t s);
+hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int st, hipStream_t s);
 
 // qkv [B*T][3D] -> q, k (optionally RMS-normalised with gains) and v^T
 struct RelayoutArgs {
