@@ -186,20 +186,26 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
         }
     }
     // online softmax per query column (lane-local except the max)
-    bf16x8 pf[2][QT];
+    float mx[QT];
+    bool grow = false;
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
-      float mx = -INFINITY;
+      float m = -INFINITY;
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) mx = fmaxf(mx, s[kt][qt][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      // move m when this tile raises some query's max by more than 8 (the
-      // branch is wave-uniform), and always on the first tile
-      if (first || __builtin_amdgcn_ballot_w64(mx > 8.0f) != 0) {
-        const float delta = first ? mx : fmaxf(mx, 0.f);
+        for (int r = 0; r < 4; ++r) m = fmaxf(m, s[kt][qt][r]);
+      m = fmaxf(m, __shfl_xor(m, 16, 64));
+      m = fmaxf(m, __shfl_xor(m, 32, 64));
+      mx[qt] = m;
+      grow = grow || m > 8.0f;
+    }
+    // move m when this tile raises some query's max by more than 8 (one
+    // wave-uniform branch for all query tiles), and always on the first tile
+    if (first || __builtin_amdgcn_ballot_w64(grow) != 0) {
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        const float delta = first ? mx[qt] : fmaxf(mx[qt], 0.f);
         // first tile: O and l are still zero, any finite factor keeps them so
         const float corr = __builtin_amdgcn_exp2f(fminf(-delta, 0.f));
         mrun[qt] += delta;
@@ -209,35 +215,34 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt) s[kt][qt] -= delta;
       }
+    }
+    // V^T operands: with the stored key order the eight keys of slot (c, g)
+    // are chunk 4c + g of the V^T row
+    bf16x8 vf[4][2];
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        vf[d][c] = *reinterpret_cast<const bf16x8*>(st + (64 + d * 16 + lr) * kDh + (((4 * c + g) ^ sw) * 8));
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
       // B operand of O^T += V^T P^T for key chunk c: slots 0-3 = key tile 2c,
       // slots 4-7 = key tile 2c+1 (keys 4g+r within each)
+      bf16x8 pf[2];
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        bf16x8 v;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          v[r] = static_cast<bf16>(__builtin_amdgcn_exp2f(s[2 * c][qt][r]));
-          v[4 + r] = static_cast<bf16>(__builtin_amdgcn_exp2f(s[2 * c + 1][qt][r]));
+          pf[c][r] = static_cast<bf16>(__builtin_amdgcn_exp2f(s[2 * c][qt][r]));
+          pf[c][4 + r] = static_cast<bf16>(__builtin_amdgcn_exp2f(s[2 * c + 1][qt][r]));
         }
-        pf[c][qt] = v;
       }
-    }
-    // O^T[dh][q] += V^T[dh][keys] P^T[keys][q]: with the stored key order the
-    // eight keys of slot (c, g) are chunk 4c + g of the V^T row; the ones
-    // operand adds the column sums of P^T into l
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt) l[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[c][qt], l[qt], 0, 0, 0);
-#pragma unroll
-    for (int d = 0; d < 4; ++d) {
-      const bf16* vrow = st + (64 + d * 16 + lr) * kDh;
+      // the ones operand adds the column sums of P^T into l
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vrow + (((4 * c + g) ^ sw) * 8));
+        l[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[c], l[qt], 0, 0, 0);
 #pragma unroll
-        for (int qt = 0; qt < QT; ++qt)
-          o[d][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[c][qt], o[d][qt], 0, 0, 0);
+        for (int d = 0; d < 4; ++d) o[d][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[d][c], pf[c], o[d][qt], 0, 0, 0);
       }
     }
   };

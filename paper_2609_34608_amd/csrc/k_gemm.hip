@@ -25,6 +25,11 @@ constexpr TileCfg kCfgs[] = {
     {128, 256, 2, 4, 4},  // 7
     {128, 128, 2, 4, 4},  // 8
     {64, 256, 1, 4, 4},   // 9
+    {64, 64, 2, 2, 8},    // 10
+    {64, 128, 2, 2, 8},   // 11
+    {128, 64, 2, 2, 8},   // 12
+    {64, 64, 2, 2, 12},   // 13
+    {128, 128, 2, 2, 8},  // 14
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
@@ -46,7 +51,12 @@ hipError_t launch_role(const GemmArgs& a, int cfg, int splits, hipStream_t s) {
     case 6: return launch_c<6, ROLE>(a, splits, s);
     case 7: return launch_c<7, ROLE>(a, splits, s);
     case 8: return launch_c<8, ROLE>(a, splits, s);
-    default: return launch_c<9, ROLE>(a, splits, s);
+    case 9: return launch_c<9, ROLE>(a, splits, s);
+    case 10: return launch_c<10, ROLE>(a, splits, s);
+    case 11: return launch_c<11, ROLE>(a, splits, s);
+    case 12: return launch_c<12, ROLE>(a, splits, s);
+    case 13: return launch_c<13, ROLE>(a, splits, s);
+    default: return launch_c<14, ROLE>(a, splits, s);
   }
 }
 
@@ -120,16 +130,22 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs a) {
 int gemm_num_configs() { return kNumCfgs; }
 
 GemmPlan plan_gemm(int M, int N, int K, int epi) {
-  // 256x256 tiles with 8 waves (128x64 each) once M gives enough tile rows;
-  // below that 64x64 tiles (64x128 for the QKV epilogue, which needs whole
-  // heads per wave); a K split only for grids under half a block per CU.
+  // From a sweep of every configuration at the workload shapes.  Large M:
+  // 256x256 tiles, 8 waves of 64x128 for wide outputs, of 128x64 otherwise.
+  // Small M: 64x64 tiles (64x128 for the QKV epilogue, which needs whole
+  // heads per wave; 128x128 over 8 waves for wide, short-K outputs); a K split
+  // only for grids under half a block per CU.
   GemmPlan p{0, 1};
   if (M >= 2048 && N % 256 == 0) {
-    p.cfg = 4;
+    p.cfg = N >= 3072 ? 5 : 4;
     return p;
   }
   if (epi == EPI_QKV) {
     p.cfg = N % 128 == 0 ? 1 : 3;
+    return p;
+  }
+  if (N >= 2048 && N % 128 == 0 && K <= 1024) {
+    p.cfg = 8;
     return p;
   }
   const long blocks = (long)((M + 63) / 64) * (N / 64);
