@@ -71,6 +71,11 @@ class RRProfile:
     gamma_cos: float = 0.80
     gamma_fit: float = 0.60
     mode: int = RR_AUTO
+    # False: the two jointly executed branches (video + observation rows,
+    # action rows) each get an alpha and must both pass (Sec. 3.3, joint
+    # execution).  True: the model's whole token set is one branch, as for each
+    # model of an independently executed pair (Sec. 3.3, independent execution).
+    single: bool = False
 
     def validate(self, L: int):
         if self.mode != RR_OFF and not (0 < self.q < self.s < self.e < L):
@@ -84,6 +89,8 @@ class RRProfile:
 def rr_alpha(p_i, p_a, eps, alpha_min, alpha_max) -> float:
     """Eq.(crr-alpha): clamp(mean(p_i*p_a) / max(mean(p_a*p_a), eps), amin, amax)."""
     p_i, p_a = dit.as64(p_i).ravel(), dit.as64(p_a).ravel()
+    if p_i.size == 0:  # an empty branch: nothing to rescale (and its gate fails)
+        return float(alpha_min)
     num = np.mean(p_i * p_a)
     den = max(np.mean(p_a * p_a), eps)
     return float(np.clip(num / den, alpha_min, alpha_max))
@@ -114,9 +121,21 @@ def rr_gate(cos, fit, gamma_cos, gamma_fit, p_a_zero=False) -> bool:
     return bool(cos >= gamma_cos and fit <= gamma_fit)
 
 
-def branch_rows(spec):
-    """Row indices (within one sample) of the two jointly executed branches:
-    V = video and observation rows, A = action rows."""
+def rr_branch_stats(p_i, p_a, prof: RRProfile):
+    """alpha (Eq. crr-alpha), cos and relative fit (Eq. crr-gate) of one
+    branch of one sample, and whether it passes the gate."""
+    alpha = rr_alpha(p_i, p_a, prof.eps, prof.alpha_min, prof.alpha_max)
+    cos = rr_cos(p_i, p_a)
+    fit = rr_fit(p_i, p_a, alpha)
+    return alpha, cos, fit, rr_gate(cos, fit, prof.gamma_cos, prof.gamma_fit, p_a_zero=not np.any(p_a))
+
+
+def branch_rows(spec, single: bool = False):
+    """Row indices (within one sample) of the branches RR checks: the two
+    jointly executed ones, V = video and observation rows and A = action rows,
+    or (single) all rows as one branch."""
+    if single:
+        return (np.arange(spec.T),)
     v = np.r_[0:spec.Nv, spec.Nv + spec.Na:spec.T]
     a = np.arange(spec.Nv, spec.Nv + spec.Na)
     return v, a
@@ -178,19 +197,17 @@ def velocity_rr(W, spec, x, cond, sigma, prof: RRProfile | None, state: LayerSta
     if state.valid and prof.mode in (RR_AUTO, RR_FORCE_SKIP):
         info.attempted = True
         B = spec.B
-        rows = branch_rows(spec)
-        alpha = np.zeros((B, 2))
-        cosv = np.zeros((B, 2))
-        fitv = np.zeros((B, 2))
+        rows = branch_rows(spec, prof.single)
+        # [B, 2] statistics; with a single branch column 1 stays NaN (no branch)
+        alpha = np.full((B, 2), np.nan)
+        cosv = np.full((B, 2), np.nan)
+        fitv = np.full((B, 2), np.nan)
         ok = True
         for b in range(B):
             for br, r in enumerate(rows):
-                pi_b, pa_b = p_i[b, r], state.p_a[b, r]
-                alpha[b, br] = rr_alpha(pi_b, pa_b, prof.eps, prof.alpha_min, prof.alpha_max)
-                cosv[b, br] = rr_cos(pi_b, pa_b)
-                fitv[b, br] = rr_fit(pi_b, pa_b, alpha[b, br])
-                ok &= rr_gate(cosv[b, br], fitv[b, br], prof.gamma_cos, prof.gamma_fit,
-                              p_a_zero=not np.any(pa_b))
+                alpha[b, br], cosv[b, br], fitv[b, br], passed = rr_branch_stats(
+                    p_i[b, r], state.p_a[b, r], prof)
+                ok &= passed
         info.alpha, info.cos, info.fit = alpha, cosv, fitv
         if forced is not None:
             accept = bool(forced.popleft())
@@ -203,7 +220,7 @@ def velocity_rr(W, spec, x, cond, sigma, prof: RRProfile | None, state: LayerSta
         # Eq.(residual-injection): h_e = h_s + alpha R_a, per sample and branch.
         h_e = h_s.copy()
         for b in range(spec.B):
-            for br, r in enumerate(branch_rows(spec)):
+            for br, r in enumerate(branch_rows(spec, prof.single)):
                 h_e[b, r] = h_s[b, r] + info.alpha[b, br] * state.R_a[b, r]
         info.accepted = True
         info.layers_skipped = e - s
@@ -247,8 +264,11 @@ def _branches(spec, x):
 
 
 def unit_rms(v):
-    """N(v) = v / sqrt(mean(v^2)) (Eq. app-transport-rms); 0 if v is zero."""
+    """N(v) = v / sqrt(mean(v^2)) (Eq. app-transport-rms); 0 if v is zero; an
+    empty branch (a model without video or without action tokens) stays empty."""
     v = dit.as64(v)
+    if v.size == 0:
+        return v.copy()
     r = np.sqrt(np.mean(v * v))
     return v / r if r > 0 else np.zeros_like(v)
 
@@ -457,6 +477,57 @@ class ReplanRuntime:
         self.x_bar, self.x_r = x, xr
         steps = len(all_infos)
         return x, ReplanInfo(path, S, self.kappa, steps, all_infos)
+
+
+# --------------------------------------------------------------------------
+# independent execution of the video and action branches (Sec. 3.3; the
+# Fast-WAM-IDM profiles of the appendix)
+# --------------------------------------------------------------------------
+def pack_condition(obs, ctx, Co: int):
+    """Condition tokens of the action model of an independently executed pair:
+    the observation tokens followed by the video model's latent tokens (the
+    action model reads the predicted video), each zero-padded to Co channels.
+    obs [B, n_obs, c_obs], ctx [B, n_ctx, c_ctx] -> [B, n_obs + n_ctx, Co]."""
+    obs, ctx = dit.as64(obs), dit.as64(ctx)
+    B, n_obs, c_obs = obs.shape
+    _, n_ctx, c_ctx = ctx.shape
+    if c_obs > Co or c_ctx > Co:
+        raise ValueError("channels exceed Co")
+    out = np.zeros((B, n_obs + n_ctx, Co))
+    out[:, :n_obs, :c_obs] = obs
+    out[:, n_obs:, :c_ctx] = ctx
+    return out
+
+
+class IdmPairRuntime:
+    """Video and action executed as two models with their own replan state,
+    schedule and RR decision.  Each control step runs the video model's
+    replan under the observation, then the action model's under the
+    observation plus the video model's new latent."""
+
+    def __init__(self, video: ReplanRuntime, action: ReplanRuntime):
+        sv, sa = video.spec, action.spec
+        if sv.Na != 0 or sa.Nv != 0:
+            raise ValueError("video model has no action tokens, action model no video tokens")
+        if sa.No < sv.Nv or sa.Co < max(sv.Co, sv.Cv):
+            raise ValueError("action condition must hold the observation and the video tokens")
+        if action.p.or_enabled:
+            raise ValueError("the action model runs under the real observation only")
+        self.video, self.action = video, action
+
+    def action_condition(self, obs, x_video):
+        sv = self.video.spec
+        ctx = dit.split_trajectory(sv, x_video)[0]
+        return pack_condition(obs, ctx, self.action.spec.Co)
+
+    def replan(self, obs_real, obs_pred=None, u_hat=None, u=None, deltas=None, weights=None,
+               noise_first=(None, None), noise_remap=(None, None), forced=(None, None)):
+        xv, info_v = self.video.replan(obs_real, obs_pred, u_hat, u, deltas, weights,
+                                       noise_first[0], noise_remap[0], forced[0])
+        cond_a = self.action_condition(obs_real, xv)
+        xa, info_a = self.action.replan(cond_a, None, None, None, None, None,
+                                        noise_first[1], noise_remap[1], forced[1])
+        return xv, xa, info_v, info_a
 
 
 def action_chunk(spec, x):

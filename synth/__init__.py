@@ -5,7 +5,7 @@ tokens and their autoregressive evolution.  It contains none of the method's
 arithmetic (no layers, no solver, no adaptation operator), so the CPU oracle
 and the GPU path can both consume its output without sharing any code.
 """
-from .workloads import WorkloadSpec, WORKLOADS, get_workload
+from .workloads import WorkloadSpec, WORKLOADS, get_pair, get_workload
 from .gen import (
     weight_manifest,
     make_weights,
@@ -18,6 +18,7 @@ from .gen import (
 __all__ = [
     "WorkloadSpec",
     "WORKLOADS",
+    "get_pair",
     "get_workload",
     "weight_manifest",
     "make_weights",

@@ -148,6 +148,39 @@ TINY_REPLAY = _reg(TINY_RR.replace(
     or_k1=1, notes="tiny closed-loop replay for tests"))
 
 
+# Independent execution of the video and action branches (Sec. 3.3, the
+# Fast-WAM-IDM profiles of the appendix): two models of the small model's
+# shape.  Video model: 768 latent + 64 observation tokens, TR from stage 5 into
+# stage 4 without a shift, anticipatory prefix 2 + 4 steps, refresh 6.  Action
+# model: 32 action tokens conditioned on the 64 observation tokens and the
+# video model's 768 latent tokens (condition channels 16), TR into stage 5
+# shifted by ten positions, 5 steps under the real observation on every later
+# replan.
+IDM_VIDEO = _reg(SMALL.replace(
+    name="idm_video", Na=0, A=1, tr_b0=4, tr_r=5, shift_action=0, or_k1=2, control_steps=100,
+    notes="video model of the independent pair (small shape, no action tokens)"))
+IDM_ACTION = _reg(SMALL.replace(
+    name="idm_action", Nv=0, No=64 + 768, Co=16, tr_b0=5, tr_r=5, shift_action=10, or_k1=0,
+    control_steps=100, seed=1,
+    notes="action model of the independent pair (conditioned on observation + video latent)"))
+
+# Tiny fp32 pair for parity tests (4 layers so RR applies; K = 4).
+TINY_IDM_VIDEO = _reg(TINY_RR.replace(
+    name="tiny_idm_video", Na=0, A=1, tr_b0=1, tr_r=2, or_k1=1, control_steps=6,
+    notes="tiny video model of the independent pair"))
+TINY_IDM_ACTION = _reg(TINY_RR.replace(
+    name="tiny_idm_action", Nv=0, No=8 + 64, Co=16, tr_b0=2, tr_r=2, shift_action=4, or_k1=0,
+    control_steps=6, seed=1, notes="tiny action model of the independent pair"))
+
+PAIRS = {"idm": ("idm_video", "idm_action"), "tiny_idm": ("tiny_idm_video", "tiny_idm_action")}
+
+
+def get_pair(name: str) -> tuple:
+    """(video spec, action spec) of an independently executed pair."""
+    v, a = PAIRS[name]
+    return WORKLOADS[v], WORKLOADS[a]
+
+
 def get_workload(name: str) -> WorkloadSpec:
     try:
         return WORKLOADS[name]
