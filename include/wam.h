@@ -69,6 +69,9 @@ extern "C" {
 #define WAM_RR_AUTO 1       /* gate of Eq. crr-gate decides reuse or refresh  */
 #define WAM_RR_FORCE_SKIP 2 /* reuse whenever a layer state exists            */
 #define WAM_RR_FORCE_FULL 3 /* always compute the middle and refresh          */
+/* wam_rr_profile.branches */
+#define WAM_RR_JOINT 0  /* video (+ observation) and action rows: two checks */
+#define WAM_RR_SINGLE 1 /* all rows: one check                                */
 
 /* ---- wam_adapt_state operations ---------------------------------------- */
 #define WAM_ADAPT_REMAP 1       /* args: const wam_remap_args*               */
@@ -113,7 +116,9 @@ typedef struct wam_handle *wam_t;
 
 /* Model configuration.  D % 64 == 0 (D <= 2048), D % H == 0, head size D/H in
  * {32, 64}, Cv <= 16, A <= 16, Co <= 64; bf16 mode additionally needs
- * D/H == 64, D % 128 == 0 and F % 128 == 0. */
+ * D/H == 64, D % 128 == 0 and F % 128 == 0.  Nv >= 0, Na >= 0, Nv + Na >= 1:
+ * a model of an independently executed pair has only video (Na = 0) or only
+ * action (Nv = 0) tokens; Cv and A stay >= 1 (their weights exist). */
 typedef struct {
   int32_t B;       /* batch (samples denoised together), 1..WAM_MAX_BATCH */
   int32_t L;       /* DiT layers                                            */
@@ -136,10 +141,18 @@ typedef struct {
   int32_t mode; /* WAM_RR_* */
   float alpha_min, alpha_max, eps;
   float gamma_cos, gamma_fit;
+  /* WAM_RR_JOINT: the jointly executed video (+ observation) and action
+   * branches each get an alpha, and the middle is skipped only when both
+   * pass (Sec. 3.3, joint execution).  WAM_RR_SINGLE: the model's whole token
+   * set is one branch, as for each model of an independently executed video /
+   * action pair (Sec. 3.3, independent execution; the branch-1 statistics of
+   * wam_step_info are then NaN). */
+  int32_t branches;
 } wam_rr_profile;
 
 /* Per-denoising-step report.  alpha/cos/fit are per sample and per branch
- * (branch 0 = video and observation rows, 1 = action rows); valid when
+ * (branch 0 = video and observation rows, 1 = action rows; with
+ * WAM_RR_SINGLE branch 0 = all rows and branch 1 = NaN); valid when
  * rr_attempted. */
 typedef struct {
   int32_t rr_active;    /* RR mode was not OFF                              */
@@ -272,6 +285,16 @@ int wam_adapt_state(wam_t h, int op, const void *args);
 int wam_consistency_score(wam_t h, int n_components, const float *const *u_hat,
                           const float *const *u, const int64_t *n, const double *delta,
                           const double *weight, double *S_out);
+/* Condition tokens of the action model of an independently executed video /
+ * action pair (Sec. 3.3; the action model reads the observation and the video
+ * model's latent): cond [B][No][Co] = the n_obs observation tokens obs
+ * [B][n_obs][c_obs] followed by the n_ctx tokens of ctx (sample b, token j,
+ * channel c at ctx[b * ctx_stride + j * c_ctx + c], e.g. the video part of
+ * the video model's trajectory), each zero-padded to Co channels.  Needs
+ * n_obs + n_ctx == No and c_obs, c_ctx <= Co.  Device pointers, caller-owned;
+ * enqueued on the handle's stream (no synchronisation). */
+int wam_pack_condition(wam_t h, const float *obs, int n_obs, int c_obs, const float *ctx, int n_ctx,
+                       int c_ctx, int64_t ctx_stride, float *cond);
 /* One replan of the joint runtime.  The first call (or after RESET_ALL) runs
  * the native K steps from noise_first; later calls apply Trajectory
  * Remapping, the anticipatory prefix under cond_pred, the consistency check

@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(_PKG, "lib", "libwam.so")
 WAM_OK, WAM_E_ARG, WAM_E_SHAPE, WAM_E_STATE, WAM_E_HIP, WAM_E_WORKSPACE, WAM_E_UNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
 WAM_FP32, WAM_BF16 = 0, 1
 WAM_RR_OFF, WAM_RR_AUTO, WAM_RR_FORCE_SKIP, WAM_RR_FORCE_FULL = 0, 1, 2, 3
+WAM_RR_JOINT, WAM_RR_SINGLE = 0, 1
 WAM_ADAPT_REMAP, WAM_ADAPT_RESET_LAYER, WAM_ADAPT_RESET_ALL, WAM_ADAPT_SET_REPLAN = 1, 2, 3, 4
 WAM_PATH_FIRST, WAM_PATH_ACCEPT, WAM_PATH_REJECT, WAM_PATH_FORCED, WAM_PATH_DIRECT = 0, 1, 2, 3, 4
 WAM_MAX_BATCH, WAM_MAX_COMPONENTS, WAM_MAX_STEPS = 16, 8, 64
@@ -34,7 +35,7 @@ class WamConfig(C.Structure):
 class WamRRProfile(C.Structure):
     _fields_ = [("q", C.c_int32), ("s", C.c_int32), ("e", C.c_int32), ("mode", C.c_int32),
                 ("alpha_min", C.c_float), ("alpha_max", C.c_float), ("eps", C.c_float),
-                ("gamma_cos", C.c_float), ("gamma_fit", C.c_float)]
+                ("gamma_cos", C.c_float), ("gamma_fit", C.c_float), ("branches", C.c_int32)]
 
 
 class WamStepInfo(C.Structure):
@@ -98,6 +99,8 @@ EXPORTS = {
     "wam_consistency_score": (C.c_int, [C.c_void_p, C.c_int, C.POINTER(C.c_void_p), C.POINTER(C.c_void_p),
                                         C.POINTER(C.c_int64), C.POINTER(C.c_double), C.POINTER(C.c_double),
                                         C.POINTER(C.c_double)]),
+    "wam_pack_condition": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int, C.c_int, C.c_void_p, C.c_int, C.c_int,
+                                     C.c_int64, C.c_void_p]),
     "wam_replan": (C.c_int, [C.c_void_p, C.POINTER(WamReplanArgs), C.POINTER(WamReplanInfo)]),
     "wam_replan_begin": (C.c_int, [C.c_void_p, C.POINTER(WamReplanArgs)]),
     "wam_replan_end": (C.c_int, [C.c_void_p, C.POINTER(WamReplanArgs), C.POINTER(WamReplanInfo)]),

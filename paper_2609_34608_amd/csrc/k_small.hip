@@ -405,13 +405,13 @@ __global__ void rr_refresh_kernel(const float* __restrict__ h, const float* __re
 
 // Device-side reuse decision: AND of the pass bits over samples and branches
 // (or forced), written as a flag that predicates the following launches.
-__global__ void rr_decide_kernel(const double* __restrict__ result, int B, int force_accept, int* flag,
+__global__ void rr_decide_kernel(const double* __restrict__ result, int B, int nbranch, int force_accept, int* flag,
                                  double* hist_stats, int* hist_flag) {
   if (threadIdx.x != 0) return;
   int all = 1;
   for (int i = 0; i < B * 2; ++i) {
     const double* r = result + (size_t)i * 8;
-    all &= r[6] != 0.0;
+    if (i % 2 < nbranch) all &= r[6] != 0.0;
     hist_stats[i * 3 + 0] = r[3];
     hist_stats[i * 3 + 1] = r[4];
     hist_stats[i * 3 + 2] = r[5];
@@ -419,6 +419,26 @@ __global__ void rr_decide_kernel(const double* __restrict__ result, int B, int f
   const int accept = force_accept ? 1 : all;
   *flag = accept;
   *hist_flag = accept;
+}
+
+// Condition of the action model of an independent pair: observation tokens,
+// then context tokens (e.g. the video model's latent), zero-padded to Co.
+__global__ void pack_condition_kernel(const float* __restrict__ obs, int n_obs, int c_obs,
+                                      const float* __restrict__ ctx, int n_ctx, int c_ctx, int64_t ctx_stride,
+                                      float* __restrict__ cond, int B, int Co) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int nt = n_obs + n_ctx;
+  if (i >= (int64_t)B * nt * Co) return;
+  const int c = (int)(i % Co);
+  const int t = (int)((i / Co) % nt);
+  const int b = (int)(i / ((int64_t)Co * nt));
+  float v = 0.f;
+  if (t < n_obs) {
+    if (c < c_obs) v = obs[((int64_t)b * n_obs + t) * c_obs + c];
+  } else if (c < c_ctx) {
+    v = ctx[(int64_t)b * ctx_stride + (int64_t)(t - n_obs) * c_ctx + c];
+  }
+  cond[i] = v;
 }
 
 __global__ void copy_f32_kernel(const float* __restrict__ src, float* __restrict__ dst, int64_t n) {
@@ -574,9 +594,18 @@ hipError_t launch_rr_refresh(const float* h, const float* hq, float* Ra, int64_t
   return hipGetLastError();
 }
 
-hipError_t launch_rr_decide(const double* result, int B, int force_accept, int* flag, double* hist_stats,
-                            int* hist_flag, hipStream_t s) {
-  launch_k(rr_decide_kernel, 1, 64, 0, s, result, B, force_accept, flag, hist_stats, hist_flag);
+hipError_t launch_rr_decide(const double* result, int B, int nbranch, int force_accept, int* flag,
+                            double* hist_stats, int* hist_flag, hipStream_t s) {
+  launch_k(rr_decide_kernel, 1, 64, 0, s, result, B, nbranch, force_accept, flag, hist_stats, hist_flag);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_condition(const float* obs, int n_obs, int c_obs, const float* ctx, int n_ctx, int c_ctx,
+                                 int64_t ctx_stride, float* cond, int B, int Co, hipStream_t s) {
+  const int64_t n = (int64_t)B * (n_obs + n_ctx) * Co;
+  if (n == 0) return hipSuccess;
+  launch_k(pack_condition_kernel, (unsigned)((n + 255) / 256), 256, 0, s, obs, n_obs, c_obs, ctx, n_ctx, c_ctx,
+           ctx_stride, cond, B, Co);
   return hipGetLastError();
 }
 

@@ -45,7 +45,7 @@ int make_dims(const wam_config* c, Dims* d, std::string* why) {
   }
   if (c->B < 1 || c->B > WAM_MAX_BATCH) return bad("B must be in 1..WAM_MAX_BATCH");
   if (c->L < 1 || c->D < 64 || c->H < 1 || c->F < 64) return bad("L, D, H, F out of range");
-  if (c->Nv < 0 || c->Na < 1 || c->No < 0 || c->Cv < 1 || c->A < 1 || c->Co < 1)
+  if (c->Nv < 0 || c->Na < 0 || c->Nv + c->Na < 1 || c->No < 0 || c->Cv < 1 || c->A < 1 || c->Co < 1)
     return bad("token counts / channels out of range");
   if (c->Cv > 16 || c->A > 16 || c->Co > 64) return bad("Cv and A must be <= 16, Co <= 64");
   if (c->D % c->H) return bad("D must be divisible by H");
@@ -414,7 +414,19 @@ int check_rr(wam_t h, const wam_rr_profile* rr) {
     return fail(h, WAM_E_ARG, "RR needs 0 < q < s < e < L");
   if (!(rr->alpha_min <= rr->alpha_max) || !(rr->eps > 0.f))
     return fail(h, WAM_E_ARG, "RR needs alpha_min <= alpha_max and eps > 0");
+  if (rr->branches != WAM_RR_JOINT && rr->branches != WAM_RR_SINGLE)
+    return fail(h, WAM_E_ARG, "RR branches must be WAM_RR_JOINT or WAM_RR_SINGLE");
   return WAM_OK;
+}
+
+// Rows of RR branch 1 as the gate / inject kernels see them: [nv, nv + na)
+// is branch 1, every other row branch 0.  A single branch puts all rows in 0.
+struct RRRows {
+  int nv, na, nbranch;
+};
+RRRows rr_rows(const Dims& d, const wam_rr_profile* rr) {
+  if (rr->branches == WAM_RR_SINGLE) return RRRows{d.T, 0, 1};
+  return RRRows{d.Nv, d.Na, 2};
 }
 
 // Final layer + heads: velocity into v_out and/or Euler update of x_euler.
@@ -456,19 +468,21 @@ int enqueue_step_device(wam_t h, int k, const float* x, const float* cond, float
   if ((st = run_layers(h, rr->q, rr->s))) return st;
   const int* flag = nullptr;
   if (attempt) {
+    const RRRows br = rr_rows(d, rr);
     RRGateArgs g{hh, h->S(ws.hq), h->S(ws.pa), h->S<double>(ws.rr_rows), h->S<double>(ws.rr_res),
-                 d.B, d.T, d.D, d.Nv, d.Na, rr->alpha_min, rr->alpha_max, rr->eps, rr->gamma_cos,
+                 d.B, d.T, d.D, br.nv, br.na, rr->alpha_min, rr->alpha_max, rr->eps, rr->gamma_cos,
                  rr->gamma_fit};
     {
       ProfScope ps(h, WAM_KC_RR_GATE, 3.0 * MD * 4);
       HIPCHK(h, launch_rr_gate(g, s));
     }
-    HIPCHK(h, launch_rr_decide(h->S<double>(ws.rr_res), d.B, rr->mode == WAM_RR_FORCE_SKIP, h->S<int>(ws.rr_flag),
-                               h->S<double>(ws.hist_stats) + (size_t)k * d.B * 6, h->S<int>(ws.hist_flag) + k, s));
+    HIPCHK(h, launch_rr_decide(h->S<double>(ws.rr_res), d.B, br.nbranch, rr->mode == WAM_RR_FORCE_SKIP,
+                               h->S<int>(ws.rr_flag), h->S<double>(ws.hist_stats) + (size_t)k * d.B * 6,
+                               h->S<int>(ws.hist_flag) + k, s));
     flag = h->S<int>(ws.rr_flag);
     {
       ProfScope ps(h, WAM_KC_RR_INJECT, 3.0 * MD * 4);
-      HIPCHK(h, launch_rr_inject(hh, h->S(ws.Ra), h->S<double>(ws.rr_res), d.B, d.T, d.D, d.Nv, d.Na, s, flag));
+      HIPCHK(h, launch_rr_inject(hh, h->S(ws.Ra), h->S<double>(ws.rr_res), d.B, d.T, d.D, br.nv, br.na, s, flag));
     }
   }
   HIPCHK(h, launch_rr_pre_middle(hh, h->S(ws.hq), h->S(ws.pa), MD, s, flag));
@@ -567,10 +581,11 @@ int forward(wam_t h, int k, const float* x, const float* cond, float* v_out, flo
     HIPCHK(h, launch_copy_f32(hh, h->S(ws.hq), MD, s));
     if ((st = run_layers(h, rr->q, rr->s))) return st;
     bool accept = false;
+    const RRRows br = rr_rows(d, rr);
     if (h->layer_valid && (rr->mode == WAM_RR_AUTO || rr->mode == WAM_RR_FORCE_SKIP)) {
       in->rr_attempted = 1;
       RRGateArgs g{hh, h->S(ws.hq), h->S(ws.pa), h->S<double>(ws.rr_rows), h->S<double>(ws.rr_res),
-                   d.B, d.T, d.D, d.Nv, d.Na, rr->alpha_min, rr->alpha_max, rr->eps, rr->gamma_cos,
+                   d.B, d.T, d.D, br.nv, br.na, rr->alpha_min, rr->alpha_max, rr->eps, rr->gamma_cos,
                    rr->gamma_fit};
       {
         ProfScope ps(h, WAM_KC_RR_GATE, 3.0 * MD * 4);
@@ -581,18 +596,19 @@ int forward(wam_t h, int k, const float* x, const float* cond, float* v_out, flo
       HIPCHK(h, hipStreamSynchronize(s));
       bool all = true;
       for (int b = 0; b < d.B; ++b)
-        for (int br = 0; br < 2; ++br) {
-          const double* r = h->host_stage + ((size_t)b * 2 + br) * 8;
-          in->alpha[b][br] = r[3];
-          in->cos[b][br] = r[4];
-          in->fit[b][br] = r[5];
-          all = all && r[6] != 0.0;
+        for (int j = 0; j < 2; ++j) {
+          const double* r = h->host_stage + ((size_t)b * 2 + j) * 8;
+          const bool live = j < br.nbranch;
+          in->alpha[b][j] = live ? r[3] : NAN;
+          in->cos[b][j] = live ? r[4] : NAN;
+          in->fit[b][j] = live ? r[5] : NAN;
+          all = all && (!live || r[6] != 0.0);
         }
       accept = rr->mode == WAM_RR_FORCE_SKIP ? true : all;
     }
     if (accept) {
       ProfScope ps(h, WAM_KC_RR_INJECT, 3.0 * MD * 4);
-      HIPCHK(h, launch_rr_inject(hh, h->S(ws.Ra), h->S<double>(ws.rr_res), d.B, d.T, d.D, d.Nv, d.Na, s));
+      HIPCHK(h, launch_rr_inject(hh, h->S(ws.Ra), h->S<double>(ws.rr_res), d.B, d.T, d.D, br.nv, br.na, s));
       in->rr_accepted = 1;
       in->layers_skipped = rr->e - rr->s;
       in->layers_evaluated = d.L - (rr->e - rr->s);
@@ -627,11 +643,13 @@ int read_history(wam_t h, int k_from, int k_to, const wam_rr_profile* rr, wam_st
     wam_step_info& in = infos[k - k_from];
     if (!in.rr_attempted) continue;
     const double* st = stats.data() + (size_t)(k - k_from) * d.B * 6;
+    const int nbranch = rr_rows(d, rr).nbranch;
     for (int b = 0; b < d.B; ++b)
       for (int br = 0; br < 2; ++br) {
-        in.alpha[b][br] = st[(b * 2 + br) * 3 + 0];
-        in.cos[b][br] = st[(b * 2 + br) * 3 + 1];
-        in.fit[b][br] = st[(b * 2 + br) * 3 + 2];
+        const bool live = br < nbranch;
+        in.alpha[b][br] = live ? st[(b * 2 + br) * 3 + 0] : NAN;
+        in.cos[b][br] = live ? st[(b * 2 + br) * 3 + 1] : NAN;
+        in.fit[b][br] = live ? st[(b * 2 + br) * 3 + 2] : NAN;
       }
     if (flags[k - k_from] == 1) {
       in.rr_accepted = 1;
@@ -965,6 +983,22 @@ int wam_consistency_score(wam_t h, int n, const float* const* u_hat, const float
     acc += weight[m] * e2;
   }
   *S_out = sqrt(acc / wsum);
+  return WAM_OK;
+}
+
+int wam_pack_condition(wam_t h, const float* obs, int n_obs, int c_obs, const float* ctx, int n_ctx, int c_ctx,
+                       int64_t ctx_stride, float* cond) {
+  if (!h) return WAM_E_ARG;
+  const Dims& d = h->d;
+  if (n_obs < 0 || n_ctx < 0 || n_obs + n_ctx != d.No)
+    return fail(h, WAM_E_SHAPE, "pack_condition needs n_obs + n_ctx == No");
+  if (c_obs < 1 || c_ctx < 1 || c_obs > d.Co || c_ctx > d.Co)
+    return fail(h, WAM_E_SHAPE, "pack_condition needs 1 <= c_obs, c_ctx <= Co");
+  if ((n_obs > 0 && !obs) || (n_ctx > 0 && !ctx) || (d.No > 0 && !cond))
+    return fail(h, WAM_E_ARG, "pack_condition: null buffer");
+  if (n_ctx > 0 && ctx_stride < (int64_t)n_ctx * c_ctx)
+    return fail(h, WAM_E_ARG, "pack_condition: ctx_stride smaller than n_ctx * c_ctx");
+  HIPCHK(h, launch_pack_condition(obs, n_obs, c_obs, ctx, n_ctx, c_ctx, ctx_stride, cond, d.B, d.Co, h->stream));
   return WAM_OK;
 }
 

@@ -236,10 +236,13 @@ hipError_t launch_rr_pre_middle(const float* h, float* hq, float* pa, int64_t n,
 hipError_t launch_rr_refresh(const float* h, const float* hq, float* Ra, int64_t n, hipStream_t s,
                              const int* flag = nullptr);
 // Decision on the device: flag = force_accept ? 1 : AND of the (sample, branch)
-// pass bits in result; hist_stats [B][2][3] (alpha, cos, fit) and hist_flag
-// record the step for a later read-back.
-hipError_t launch_rr_decide(const double* result, int B, int force_accept, int* flag, double* hist_stats,
-                            int* hist_flag, hipStream_t s);
+// pass bits in result over the first nbranch branches; hist_stats [B][2][3]
+// (alpha, cos, fit) and hist_flag record the step for a later read-back.
+hipError_t launch_rr_decide(const double* result, int B, int nbranch, int force_accept, int* flag,
+                            double* hist_stats, int* hist_flag, hipStream_t s);
+// cond [B][n_obs + n_ctx][Co]: obs tokens then ctx tokens, zero-padded channels
+hipError_t launch_pack_condition(const float* obs, int n_obs, int c_obs, const float* ctx, int n_ctx, int c_ctx,
+                                 int64_t ctx_stride, float* cond, int B, int Co, hipStream_t s);
 // dst <- src (n floats), a kernel rather than a copy engine command
 hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t s);
 

@@ -53,9 +53,9 @@ def config_of(spec) -> abi.WamConfig:
 
 
 def rr_profile(q=0, s=0, e=0, mode=abi.WAM_RR_OFF, alpha_min=1.0, alpha_max=1.25, eps=1e-8,
-               gamma_cos=0.80, gamma_fit=0.60) -> abi.WamRRProfile:
+               gamma_cos=0.80, gamma_fit=0.60, branches=abi.WAM_RR_JOINT) -> abi.WamRRProfile:
     return abi.WamRRProfile(q=q, s=s, e=e, mode=mode, alpha_min=alpha_min, alpha_max=alpha_max, eps=eps,
-                          gamma_cos=gamma_cos, gamma_fit=gamma_fit)
+                          gamma_cos=gamma_cos, gamma_fit=gamma_fit, branches=branches)
 
 
 @dataclass
@@ -233,6 +233,14 @@ class WamModel:
         self._leave()
         return S.value
 
+    def pack_condition(self, obs, n_obs, c_obs, ctx, n_ctx, c_ctx, ctx_stride, out):
+        """out [B][No][Co] = obs tokens then ctx tokens, zero-padded (wam_pack_condition)."""
+        self._enter()
+        self._check(self.lib.wam_pack_condition(self.h, _ptr(obs), n_obs, c_obs, _ptr(ctx), n_ctx, c_ctx,
+                                                ctx_stride, _ptr(out)), "wam_pack_condition")
+        self._leave()
+        return out
+
     def replan_args(self, cond_real, x_out, noise_remap, *, cond_pred=None, u_hat=(), u=(), delta=(), weight=(),
                     noise_first=None, rr=None, b0=0, r=0, shift_action=0, shift_video=0, k1=0, tau=0.5,
                     kappa_max=3, tr_enabled=True, or_enabled=True, rr_first=True, rr_prefix=True,
@@ -291,3 +299,29 @@ class WamModel:
         t, n, w = C.c_double(), C.c_int64(), C.c_double()
         self._check(self.lib.wam_profile_read(self.h, kc, C.byref(t), C.byref(n), C.byref(w)), "wam_profile_read")
         return t.value, n.value, w.value
+
+
+class IdmPair:
+    """Independently executed video and action models (Sec. 3.3): per control
+    step the video model's replan under the observation, then the action
+    model's under the observation followed by the video model's new latent
+    (packed on the device by wam_pack_condition).  Each model keeps its own
+    replan state, schedule, RR decision and graphs."""
+
+    def __init__(self, video: WamModel, action: WamModel, n_obs: int, c_obs: int):
+        cv, ca = video.cfg, action.cfg
+        if cv.Na != 0 or ca.Nv != 0 or ca.No != n_obs + cv.Nv or ca.Co < max(c_obs, cv.Cv):
+            raise WamError("action condition must hold the observation and the video latent tokens")
+        self.video, self.action = video, action
+        self.n_obs, self.c_obs = n_obs, c_obs
+        self.cond_action = torch.zeros((ca.B, ca.No, ca.Co), dtype=torch.float32, device=action.device)
+
+    def replan(self, obs_real, x_video, x_action, noise_remap_video, noise_remap_action, video_kw=None,
+               action_kw=None):
+        """One control step; returns (video info, action info)."""
+        iv = self.video.replan(obs_real, x_video, noise_remap_video, **(video_kw or {}))
+        cv = self.video.cfg
+        self.action.pack_condition(obs_real, self.n_obs, self.c_obs, x_video, cv.Nv, cv.Cv, self.video.traj,
+                                   self.cond_action)
+        ia = self.action.replan(self.cond_action, x_action, noise_remap_action, **(action_kw or {}))
+        return iv, ia

@@ -24,16 +24,19 @@ def rel_err(got, ref):
     return float(np.max(np.abs(got - ref)) / np.max(np.abs(ref)))
 
 
-def rr_of(spec, mode, **kw):
-    """(GPU profile, oracle profile) pair with the workload's RR constants."""
-    from paper_2609_34608_amd import runtime as R
+def rr_of(spec, mode, single=False, **kw):
+    """(GPU profile, oracle profile) pair with the workload's RR constants;
+    single = one branch over all rows (independent execution)."""
+    from paper_2609_34608_amd import runtime as R, _lib as L
     q, s, e = spec.rr_bounds
     p = dict(alpha_min=spec.rr_alpha_min, alpha_max=spec.rr_alpha_max, eps=spec.rr_eps,
              gamma_cos=spec.rr_gamma_cos, gamma_fit=spec.rr_gamma_fit)
     p.update(kw)
     # the device compares in float32 thresholds; give the oracle the same values
     po = {k: float(np.float32(v)) for k, v in p.items()}
-    return R.rr_profile(q, s, e, mode, **p), OM.RRProfile(q, s, e, mode=mode, **po)
+    branches = L.WAM_RR_SINGLE if single else L.WAM_RR_JOINT
+    return (R.rr_profile(q, s, e, mode, branches=branches, **p),
+            OM.RRProfile(q, s, e, mode=mode, single=single, **po))
 
 
 def f32_sigmas(K, shift=1.0):

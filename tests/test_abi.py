@@ -56,9 +56,10 @@ def test_binding_order_matches_manifest():
         assert R.host_weight_order(w.L) == [n for n, _, _ in weight_manifest(w)]
 
 
-@pytest.mark.parametrize("bad", [dict(B=0), dict(B=17), dict(D=100), dict(H=5), dict(Na=0),
+@pytest.mark.parametrize("bad", [dict(B=0), dict(B=17), dict(D=100), dict(H=5), dict(Nv=0, Na=0), dict(Na=-1),
                                  dict(dtype="bf16", H=4), dict(Cv=17), dict(A=17), dict(Co=65), dict(ln_eps=0.0)])
 def test_invalid_configs_rejected(lib, bad):
+    """Shape limits of wam_config (include/wam.h); a model needs a trajectory."""
     base = dict(B=1, L=2, D=128, H=4, F=512, Nv=64, Cv=16, Na=16, A=7, No=8, Co=16, dtype="fp32")
     base.update(bad)
     cfg = R.make_config(**base)
@@ -87,3 +88,15 @@ def test_init_rejects_short_buffers_without_touching_device(lib):
     assert lib.wam_sync(None) == L.WAM_E_ARG
     assert lib.wam_set_schedule(None, None, 4) == L.WAM_E_ARG
     assert lib.wam_adapt_state(None, L.WAM_ADAPT_RESET_ALL, None) == L.WAM_E_ARG
+
+
+@pytest.mark.parametrize("one_branch", [dict(Na=0), dict(Nv=0)])
+def test_single_branch_configs_accepted(lib, one_branch):
+    """A model of an independently executed pair has only video or only action
+    tokens (Sec. 3.3, independent execution)."""
+    base = dict(B=1, L=2, D=128, H=4, F=512, Nv=64, Cv=16, Na=16, A=7, No=8, Co=16, dtype="fp32")
+    base.update(one_branch)
+    cfg = R.make_config(**base)
+    assert lib.wam_host_weight_count(C.byref(cfg)) > 0
+    assert lib.wam_workspace_bytes(C.byref(cfg)) > 0
+    assert lib.wam_traj_elems(C.byref(cfg)) == base["Nv"] * 16 + base["Na"] * 7

@@ -15,7 +15,14 @@ import torch.nn.functional as Fn
 from oracle import dit
 from synth import get_workload, make_weights, make_initial_noise, make_observations
 
-torch.set_default_dtype(torch.float64)
+@pytest.fixture(scope="module", autouse=True)
+def float64_default():
+    """float64 torch references in this module only (restored afterwards, so
+    that tensors created by later test modules keep torch's float32 default)."""
+    prev = torch.get_default_dtype()
+    torch.set_default_dtype(torch.float64)
+    yield
+    torch.set_default_dtype(prev)
 
 
 def t64(a):
