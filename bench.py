@@ -117,7 +117,8 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=30)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", default="replay", help="replay (small model) | mid | large")
+    p.add_argument("--workload", default="replay",
+                   help="replay (small model) | mid | large | idm (independent video / action pair)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-native", action="store_true")
     p.add_argument("--cpu-sample-steps", type=int, default=5)
@@ -146,12 +147,20 @@ def main():
     if args.ablation:
         if args.gpus != 1:
             sys.exit(2)
+        from synth.workloads import PAIRS
+        if args.workload in PAIRS:
+            print("the ablation runs on the single-model workloads", file=sys.stderr)
+            sys.exit(2)
         ablation(args)
         return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); multi-GPU runs are not part "
               "of this build.", file=sys.stderr)
         sys.exit(2)
+    from synth.workloads import PAIRS
+    if args.workload in PAIRS:
+        idm_main(args)
+        return
     import numpy as np
     import torch
 
@@ -337,6 +346,179 @@ def main():
     m.close()
 
 
+def idm_main(args):
+    """Independent execution of the video and action branches (Sec. 3.3,
+    Fast-WAM-IDM profiles): one step = one control step of the pair (video
+    replan under the observation, action replan under the observation and the
+    video latent).  value counts the denoising steps of both models."""
+    import numpy as np
+    import torch
+
+    from paper_2609_34608_amd import _lib as L
+    from paper_2609_34608_amd import runtime as R
+    from synth import get_pair, make_weights, make_initial_noise, make_observations, make_remap_noise
+
+    sv, sa = get_pair(args.workload)
+    dev = torch.device("cuda:0")
+    Wv, Wa = make_weights(sv), make_weights(sa)
+    models = [R.WamModel(R.config_of(sp), W, device=dev, own_stream=args.exec == "graph")
+              for sp, W in ((sv, Wv), (sa, Wa))]
+    mv, ma = models
+    K = sv.K
+    for m in models:
+        m.set_option(L.WAM_OPT_DEVICE_DECISION, int(args.exec in ("device", "graph")))
+        m.set_option(L.WAM_OPT_GRAPHS, int(args.exec == "graph"))
+        m.set_schedule(1.0 - np.arange(K + 1, dtype=np.float64) / K)
+    pair = R.IdmPair(mv, ma, sv.No, sv.Co)
+    modes = {"auto": L.WAM_RR_AUTO, "force_skip": L.WAM_RR_FORCE_SKIP, "force_full": L.WAM_RR_FORCE_FULL,
+             "off": L.WAM_RR_OFF}
+
+    def rrp(sp, mode):
+        q, s_, e = sp.rr_bounds
+        return R.rr_profile(q, s_, e, mode, sp.rr_alpha_min, sp.rr_alpha_max, sp.rr_eps, sp.rr_gamma_cos,
+                            sp.rr_gamma_fit, branches=L.WAM_RR_SINGLE)
+
+    rr = (rrp(sv, modes[args.rr_mode]), rrp(sa, modes[args.rr_mode]))
+    n_ctrl = 2 + args.warmup + args.steps  # first, warm-up, attribution and timed replans
+    obs = make_observations(sv, n_ctrl)
+    rho = sv.ar_rho
+    delta = 1.0 / np.sqrt(1.0 - rho * rho)
+    obs_d = torch.from_numpy(obs).to(dev)
+    pred_d = torch.from_numpy((rho * obs[:-1]).astype(np.float32)).to(dev)
+    nf = [torch.from_numpy(make_initial_noise(sp)).to(dev) for sp in (sv, sa)]
+    rn = [torch.from_numpy(np.stack([make_remap_noise(sp, t) for t in range(n_ctrl)])).to(dev) for sp in (sv, sa)]
+    xv, xa = mv.new_traj(), ma.new_traj()
+
+    def replan(t, rr=rr):
+        cr = obs_d[t]
+        cp = pred_d[t - 1] if t > 0 else cr
+        return pair.replan(
+            cr, xv, xa, rn[0][t], rn[1][t],
+            video_kw=dict(cond_pred=cp, u_hat=[cp], u=[cr], delta=[delta], weight=[1.0], noise_first=nf[0],
+                          rr=rr[0], b0=sv.tr_b0, r=sv.tr_r, shift_action=0, shift_video=sv.shift_video,
+                          k1=sv.or_k1, tau=sv.or_tau, kappa_max=sv.or_kappa_max),
+            action_kw=dict(noise_first=nf[1], rr=rr[1], b0=sa.tr_b0, r=sa.tr_r, shift_action=sa.shift_action,
+                           shift_video=0, k1=0, or_enabled=False))
+
+    t = 0
+    replan(t)
+    t += 1
+    for _ in range(args.warmup):
+        replan(t)
+        t += 1
+    classes = [L.WAM_KC_GEMM_QKV, L.WAM_KC_GEMM_PROJ, L.WAM_KC_GEMM_FC1, L.WAM_KC_GEMM_FC2, L.WAM_KC_ATTENTION]
+    for m in models:
+        for kc in classes:
+            m.profile_enable(kc, True, 4096)
+    replan(t)
+    t += 1
+    tot = {}
+    for mi, m in enumerate(models):
+        for kc in classes:
+            tot[(mi, kc)] = m.profile_read(kc)[0]
+            m.profile_enable(kc, False)
+    dmod, dom = max(tot, key=tot.get)
+    models[dmod].profile_enable(dom, True, 200000)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    infos = []
+    for _ in range(args.steps):
+        infos.append(replan(t))
+        t += 1
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    dom_ms, dom_n, dom_work = models[dmod].profile_read(dom)
+    models[dmod].profile_enable(dom, False)
+
+    steps_v = sum(iv.steps for iv, _ in infos)
+    steps_a = sum(ia.steps for _, ia in infos)
+    flops = sum(sp.flops_per_layer() * sum(i[j].steps * sp.L - i[j].layers_skipped for i in infos)
+                for j, sp in enumerate((sv, sa)))
+    dom_tflops = dom_work / (dom_ms * 1e-3) / 1e12 if dom_ms > 0 else 0.0
+
+    def reuse(j):
+        att = sum(i[j].rr_attempts for i in infos)
+        dense = sum(i[j].layers_dense for i in infos)
+        st = sum(i[j].n_start for i in infos)
+        return {"rr_accept": sum(i[j].rr_reuses for i in infos) / att if att else None,
+                "rr_skip_frac": sum(i[j].layers_skipped for i in infos) / dense if dense else None,
+                "or_accept": sum(i[j].n_bind for i in infos) / st if st else None}
+
+    name = {0: "video", 1: "action"}
+    out = {
+        "metric": "denoise steps/s + action chunks/s per MI355X; MFMA % of bf16 peak",
+        "value": round((steps_v + steps_a) / elapsed, 3),
+        "unit": "denoise steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(1000.0 * elapsed / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if sv.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded random-init weights N(0,0.02), N(0,1) noise, AR(1) observations)",
+        "config": {
+            "workload": (f"{args.workload}: independently executed video / action DiTs, closed-loop replan per "
+                         f"model (video: L{sv.L} D{sv.D} T{sv.T}, b0={sv.tr_b0} r={sv.tr_r} prefix {sv.or_k1}+"
+                         f"{K - sv.tr_b0 - sv.or_k1}; action: L{sa.L} D{sa.D} T{sa.T} (obs {sv.No} + video "
+                         f"{sv.Nv} condition tokens), b0={sa.tr_b0} shift={sa.shift_action}) K{K}, "
+                         "single-branch RR per model"),
+            "step": "one control step of the pair (video replan, then action replan)",
+            "exec": args.exec,
+        },
+        "action_chunks_per_s": round(args.steps / elapsed, 3),
+        "denoise_steps_per_replan": {"video": steps_v / args.steps, "action": steps_a / args.steps},
+        "mfma_frac_dit": round(flops / elapsed / 1e12 / MFMA_BF16_PEAK_TFLOPS, 5),
+        "dit_tflops": round(flops / elapsed / 1e12, 3),
+        "reuse_stats": {"video": reuse(0), "action": reuse(1)},
+        "roofline": {
+            "kernel": f"{name[dmod]} {L.KERNEL_CLASS_NAMES[dom]}",
+            "bound": "mfma",
+            "achieved": round(dom_tflops, 3),
+            "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(dom_tflops / MFMA_BF16_PEAK_TFLOPS, 5),
+            "traffic": lookup_traffic(args.workload, L.KERNEL_CLASS_NAMES[dom]),
+            "launches": dom_n,
+            "avg_launch_us": round(1000.0 * dom_ms / dom_n, 3) if dom_n else None,
+            "class_ms_one_replan": {f"{name[mi]} {L.KERNEL_CLASS_NAMES[k]}": round(v, 4)
+                                    for (mi, k), v in tot.items()},
+        },
+    }
+    if not args.no_native:
+        # full re-denoise of both models: K steps of video from noise, the
+        # condition packing, K steps of action
+        nrep = max(3, args.steps // 5)
+        vv, aa = mv.new_traj(), ma.new_traj()
+
+        def native(i):
+            vv.copy_(nf[0])
+            mv.continue_(0, K, vv, obs_d[i])
+            ma.pack_condition(obs_d[i], sv.No, sv.Co, vv, sv.Nv, sv.Cv, mv.traj, pair.cond_action)
+            aa.copy_(nf[1])
+            ma.continue_(0, K, aa, pair.cond_action)
+
+        for m in models:
+            m.reset_all()
+        native(0)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(nrep):
+            native(i + 1)
+        torch.cuda.synchronize()
+        nat = (time.perf_counter() - t0) / nrep
+        out["native_chunk_ms"] = round(1000.0 * nat, 4)
+        out["native_steps_per_s"] = round(2 * K / nat, 3)
+        out["reuse_latency_speedup"] = round(nat / (elapsed / args.steps), 4)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(sv, Wv, obs, args.cpu_sample_steps, single=True)
+        out["cpu_baseline"]["sample"] += " (video model of the pair)"
+    print(json.dumps(out), flush=True)
+    for m in models:
+        m.close()
+
+
 def ablation(args):
     """Closed-loop replans per variant, mirroring the paper's ablation of the
     three mechanisms and graph replay: GPU time per replan (foreground +
@@ -429,7 +611,7 @@ def ablation(args):
     m.close()
 
 
-def cpu_baseline(spec, W, obs, n_steps):
+def cpu_baseline(spec, W, obs, n_steps, single=False):
     """The float64 oracle on the host: a bounded sample of Euler steps of the
     same model (the continuation of one accepted replan), timed."""
     import numpy as np
@@ -443,7 +625,7 @@ def cpu_baseline(spec, W, obs, n_steps):
     sig = OM.flow_schedule(spec.K)
     q, s, e = spec.rr_bounds
     rr = OM.RRProfile(q, s, e, spec.rr_alpha_min, spec.rr_alpha_max, spec.rr_eps, spec.rr_gamma_cos,
-                      spec.rr_gamma_fit)
+                      spec.rr_gamma_fit, single=single)
     x = make_initial_noise(spec)
     k0 = spec.K - n_steps
     t0 = time.perf_counter()
