@@ -86,6 +86,121 @@ __device__ __forceinline__ void epi4(const GemmArgs& a, int m, int n, float v0, 
   }
 }
 
+// Epilogue of one wave's accumulators: acc[j][i] element r is the product at
+// row mb + i*16 + lane%16, column nb + j*16 + 4*(lane/16) + r.  SPLIT stores
+// the fp32 partial of K split `split`; the others apply the role's epilogue.
+template <int EPI, int TN, int TM, bool SPLIT>
+__device__ __forceinline__ void store_tile(const GemmArgs& a, const f32x4 (&acc)[TN][TM], int mb, int nb, int lane,
+                                           int split) {
+  const int lr = lane % 16, lg = lane / 16;
+  if constexpr (SPLIT) {
+    // fp32 partial tile of this K split; the role's reduce pass finishes it
+    float* P = a.partial + (size_t)split * a.M * a.N;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int m = mb + i * 16 + lr;
+      if (m >= a.M) continue;
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int n = nb + j * 16 + lg * 4;
+        *reinterpret_cast<f32x4*>(P + (size_t)m * a.N + n) = acc[j][i];
+      }
+    }
+  } else if constexpr (EPI == EPI_QKV) {
+    const QkvOut& qo = a.qkv;
+    const int D = qo.D;
+    // per-lane constants hoisted out of the store loop: bias of the lane's
+    // columns and the q / k gains of its head dims (d = jj*16 + 4*lg + r)
+    f32x4 bias[TN], qg[4], kg[4];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) bias[j] = *reinterpret_cast<const f32x4*>(a.bias + nb + j * 16 + lg * 4);
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      qg[jj] = kg[jj] = f32x4{1.f, 1.f, 1.f, 1.f};
+      if (qo.qk_norm) {
+        qg[jj] = *reinterpret_cast<const f32x4*>(qo.q_g + jj * 16 + lg * 4);
+        kg[jj] = *reinterpret_cast<const f32x4*>(qo.k_g + jj * 16 + lg * 4);
+      }
+      qg[jj] *= kQLog2Scale;  // attention scores come out in log2 units
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int m = mb + i * 16 + lr;
+      const int b = m / qo.T, t = m % qo.T;
+#pragma unroll
+      for (int hs = 0; hs < TN / 4; ++hs) {
+        const int nh = nb + hs * 64;  // first column of this head
+        const int sec = nh / D, head = (nh % D) / 64;
+        f32x4 v[4];
+        float ss = 0.f;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          v[jj] = acc[hs * 4 + jj][i] + bias[hs * 4 + jj];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) ss += v[jj][r] * v[jj][r];
+        }
+        if (sec < 2) {
+          ss += __shfl_xor(ss, 16, 64);
+          ss += __shfl_xor(ss, 32, 64);
+          const f32x4* gain = sec == 0 ? qg : kg;
+          const float rs = qo.qk_norm ? rsqrtf(ss * (1.0f / 64.0f) + qo.eps) : 1.0f;
+          if (m < a.M) {
+            bf16* dst = (sec == 0 ? qo.q : qo.k) + (((size_t)b * qo.H + head) * qo.Tpad + t) * 64;
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+              const f32x4 o = v[jj] * rs * gain[jj];
+              store_bf16x4(dst + jj * 16 + lg * 4, o[0], o[1], o[2], o[3]);
+            }
+          }
+        } else if (m < a.M) {
+          // V^T row d holds the tokens of each 64-key block in vt_key_pos order
+          bf16* dst = qo.vt + ((size_t)b * qo.H + head) * 64 * qo.Tpad + (t & ~63) + vt_key_pos(t & 63);
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              dst[(size_t)(jj * 16 + lg * 4 + r) * qo.Tpad] = static_cast<bf16>(v[jj][r]);
+        }
+      }
+    }
+  } else {
+    // bias (and gate) of this lane's columns once, in registers: the output
+    // may alias them as far as the compiler knows, so loads inside the store
+    // loop would be repeated and serialised behind every store
+    f32x4 bias[TN], gate[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int n = nb + j * 16 + lg * 4;
+      bias[j] = *reinterpret_cast<const f32x4*>(a.bias + n);
+      if constexpr (EPI == EPI_GATED_RES) gate[j] = *reinterpret_cast<const f32x4*>(a.gate + n);
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int m = mb + i * 16 + lr;
+      if (m >= a.M) continue;
+      if constexpr (EPI == EPI_GATED_RES) {
+        // residual stream h += gate * (acc + bias): all loads of the row first
+        f32x4* hrow = reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + (size_t)m * a.N + nb + lg * 4);
+        f32x4 hv[TN];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) hv[j] = hrow[j * 4];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) hrow[j * 4] = hv[j] + gate[j] * (acc[j][i] + bias[j]);
+      } else {
+        bf16* orow = static_cast<bf16*>(a.out) + (size_t)m * a.N + nb + lg * 4;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const f32x4 v = acc[j][i] + bias[j];
+          if constexpr (EPI == EPI_BIAS_GELU)
+            store_bf16x4(orow + j * 16, gelu_tanh_f(v[0]), gelu_tanh_f(v[1]), gelu_tanh_f(v[2]), gelu_tanh_f(v[3]));
+          else
+            store_bf16x4(orow + j * 16, v[0], v[1], v[2], v[3]);
+        }
+      }
+    }
+  }
+}
+
 template <int BM, int BN, int WGM, int WGN, int ST, int EPI, int ROLE, bool SPLIT>
 __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
   constexpr int NW = WGM * WGN;
@@ -190,113 +305,7 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
   // no load may still be writing this block's LDS when the block retires
   __builtin_amdgcn_s_waitcnt(0);
 
-  // accumulator (j,i) element r: row m = i*16 + lane%16, column n = j*16 + 4*(lane/16) + r
-  if constexpr (SPLIT) {
-    // fp32 partial tile of this K split; the role's reduce pass finishes it
-    float* P = a.partial + (size_t)blockIdx.z * a.M * a.N;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      const int m = m0 + wm * WM + i * 16 + lr;
-      if (m >= a.M) continue;
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int n = n0 + wn * WN + j * 16 + lg * 4;
-        *reinterpret_cast<f32x4*>(P + (size_t)m * a.N + n) = acc[j][i];
-      }
-    }
-  } else if constexpr (EPI == EPI_QKV) {
-    const QkvOut& qo = a.qkv;
-    const int D = qo.D;
-    // per-lane constants hoisted out of the store loop: bias of the lane's
-    // columns and the q / k gains of its head dims (d = jj*16 + 4*lg + r)
-    f32x4 bias[TN], qg[4], kg[4];
-#pragma unroll
-    for (int j = 0; j < TN; ++j) bias[j] = *reinterpret_cast<const f32x4*>(a.bias + n0 + wn * WN + j * 16 + lg * 4);
-#pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      qg[jj] = kg[jj] = f32x4{1.f, 1.f, 1.f, 1.f};
-      if (qo.qk_norm) {
-        qg[jj] = *reinterpret_cast<const f32x4*>(qo.q_g + jj * 16 + lg * 4);
-        kg[jj] = *reinterpret_cast<const f32x4*>(qo.k_g + jj * 16 + lg * 4);
-      }
-      qg[jj] *= kQLog2Scale;  // attention scores come out in log2 units
-    }
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      const int m = m0 + wm * WM + i * 16 + lr;
-      const int b = m / qo.T, t = m % qo.T;
-#pragma unroll
-      for (int hs = 0; hs < WN / 64; ++hs) {
-        const int nh = n0 + wn * WN + hs * 64;  // first column of this head
-        const int sec = nh / D, head = (nh % D) / 64;
-        f32x4 v[4];
-        float ss = 0.f;
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          v[jj] = acc[hs * 4 + jj][i] + bias[hs * 4 + jj];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) ss += v[jj][r] * v[jj][r];
-        }
-        if (sec < 2) {
-          ss += __shfl_xor(ss, 16, 64);
-          ss += __shfl_xor(ss, 32, 64);
-          const f32x4* gain = sec == 0 ? qg : kg;
-          const float rs = qo.qk_norm ? rsqrtf(ss * (1.0f / 64.0f) + qo.eps) : 1.0f;
-          if (m < a.M) {
-            bf16* dst = (sec == 0 ? qo.q : qo.k) + (((size_t)b * qo.H + head) * qo.Tpad + t) * 64;
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-              const f32x4 o = v[jj] * rs * gain[jj];
-              store_bf16x4(dst + jj * 16 + lg * 4, o[0], o[1], o[2], o[3]);
-            }
-          }
-        } else if (m < a.M) {
-          // V^T row d holds the tokens of each 64-key block in vt_key_pos order
-          bf16* dst = qo.vt + ((size_t)b * qo.H + head) * 64 * qo.Tpad + (t & ~63) + vt_key_pos(t & 63);
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              dst[(size_t)(jj * 16 + lg * 4 + r) * qo.Tpad] = static_cast<bf16>(v[jj][r]);
-        }
-      }
-    }
-  } else {
-    // bias (and gate) of this lane's columns once, in registers: the output
-    // may alias them as far as the compiler knows, so loads inside the store
-    // loop would be repeated and serialised behind every store
-    f32x4 bias[TN], gate[TN];
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int n = n0 + wn * WN + j * 16 + lg * 4;
-      bias[j] = *reinterpret_cast<const f32x4*>(a.bias + n);
-      if constexpr (EPI == EPI_GATED_RES) gate[j] = *reinterpret_cast<const f32x4*>(a.gate + n);
-    }
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      const int m = m0 + wm * WM + i * 16 + lr;
-      if (m >= a.M) continue;
-      if constexpr (EPI == EPI_GATED_RES) {
-        // residual stream h += gate * (acc + bias): all loads of the row first
-        f32x4* hrow = reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + (size_t)m * a.N + n0 + wn * WN + lg * 4);
-        f32x4 hv[TN];
-#pragma unroll
-        for (int j = 0; j < TN; ++j) hv[j] = hrow[j * 4];
-#pragma unroll
-        for (int j = 0; j < TN; ++j) hrow[j * 4] = hv[j] + gate[j] * (acc[j][i] + bias[j]);
-      } else {
-        bf16* orow = static_cast<bf16*>(a.out) + (size_t)m * a.N + n0 + wn * WN + lg * 4;
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const f32x4 v = acc[j][i] + bias[j];
-          if constexpr (EPI == EPI_BIAS_GELU)
-            store_bf16x4(orow + j * 16, gelu_tanh_f(v[0]), gelu_tanh_f(v[1]), gelu_tanh_f(v[2]), gelu_tanh_f(v[3]));
-          else
-            store_bf16x4(orow + j * 16, v[0], v[1], v[2], v[3]);
-        }
-      }
-    }
-  }
+  store_tile<EPI, TN, TM, SPLIT>(a, acc, m0 + wm * WM, n0 + wn * WN, lane, blockIdx.z);
 }
 
 // Split-K second pass: sum the partials in split order, then the epilogue.

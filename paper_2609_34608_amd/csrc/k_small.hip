@@ -224,13 +224,142 @@ __global__ void ln_modulate_v4_kernel(const float* __restrict__ h, const float* 
 }
 
 // ------------------------------------------------------------- final layer + Euler
-// Four trajectory rows per wave; lane = (row r = lane/16, output channel
-// o = lane%16).  The 16 lanes of a row compute its LayerNorm statistics
+// One wave per group of R trajectory rows of one branch of one sample, so the
+// rows share the branch's head weights (W^T packed [Cout][D]).  A lane holds
+// elements VEC lane + 64 VEC i .. + VEC-1 of each row.  Every load that does
+// not depend on a reduction is issued up front (the rows, the modulation) and
+// the head weights arrive one column chunk at a time for all 16 channels, so a
+// wave waits on memory only 1 + D / (64 VEC) times.  Each lane forms partial
+// products of its elements for R rows x 16 channels; butterfly sums over the
+// 64 lanes leave lane l < 16 R with the full dot product of row l / 16,
+// channel l % 16, which it stores as the velocity and/or applies as the Euler
+// update x += dsigma v.
+constexpr int kFinalCout = 16;
+template <int VEC, int R, int MAXC>
+__global__ __launch_bounds__(256) void final_kernel(FinalArgs a) {
+  using vec = float __attribute__((ext_vector_type(VEC)));
+  const int lane = threadIdx.x % kWave;
+  const int wave = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+  const int gv = (a.Nv + R - 1) / R, ga = (a.Na + R - 1) / R;
+  int b, t0, tend;
+  bool video;
+  if (wave < a.B * gv) {
+    b = wave / gv;
+    t0 = (wave % gv) * R;
+    tend = a.Nv;
+    video = true;
+  } else {
+    const int w = wave - a.B * gv;
+    if (w >= a.B * ga) return;
+    b = w / ga;
+    t0 = a.Nv + (w % ga) * R;
+    tend = a.Nv + a.Na;
+    video = false;
+  }
+  const int nch = a.D / (kWave * VEC);
+  auto col = [&](int i) { return VEC * lane + kWave * VEC * i; };
+  vec u[R][MAXC], sc[MAXC], sh[MAXC];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    // rows past the branch end re-read the group's first row (never stored)
+    const float* hr = a.h + ((size_t)b * a.T + (t0 + r < tend ? t0 + r : t0)) * a.D;
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i)
+      if (i < nch) u[r][i] = *reinterpret_cast<const vec*>(hr + col(i));
+  }
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i)
+    if (i < nch) {
+      sc[i] = *reinterpret_cast<const vec*>(a.scale + col(i));
+      sh[i] = *reinterpret_cast<const vec*>(a.shift + col(i));
+    }
+  float mean[R], rstd[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i)
+      if (i < nch)
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) s += u[r][i][j];
+    mean[r] = wave_sum(s) / (float)a.D;
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    float q = 0.f;
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i)
+      if (i < nch)
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+          const float dv = u[r][i][j] - mean[r];
+          q += dv * dv;
+        }
+    rstd[r] = rsqrtf(wave_sum(q) / (float)a.D + a.eps);
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r)
+#pragma unroll
+    for (int i = 0; i < MAXC; ++i)
+      if (i < nch) u[r][i] = (u[r][i] - mean[r]) * rstd[r] * (1.0f + sc[i]) + sh[i];
+  const int cout = video ? a.Cv : a.A;
+  const float* W = video ? a.wv : a.wa;
+  constexpr int NV = R * kFinalCout;  // partial sums per lane, index r * 16 + o
+  float v[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) v[j] = 0.f;
+#pragma unroll
+  for (int i = 0; i < MAXC; ++i) {
+    if (i < nch) {
+      vec w[kFinalCout];
+#pragma unroll
+      for (int o = 0; o < kFinalCout; ++o)
+        w[o] = o < cout ? *reinterpret_cast<const vec*>(W + (size_t)o * a.D + col(i)) : vec(0.f);
+#pragma unroll
+      for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int o = 0; o < kFinalCout; ++o) {
+          const vec p = u[r][i] * w[o];
+#pragma unroll
+          for (int j = 0; j < VEC; ++j) v[r * kFinalCout + o] += p[j];
+        }
+    }
+  }
+  // lane bits above NV: plain butterfly sums; then a reduce-scatter, where
+  // after the step over lane bit s, v[j] (j < s) holds the partial sum of
+  // index j + (lane & s) + the bits already consumed.  Lane l ends with the
+  // full sum of index l % NV.
+#pragma unroll
+  for (int s = kWave / 2; s >= NV; s >>= 1)
+#pragma unroll
+    for (int j = 0; j < NV; ++j) v[j] += __shfl_xor(v[j], s, 64);
+#pragma unroll
+  for (int s = NV / 2; s >= 1; s >>= 1) {
+    const bool hi = (lane & s) != 0;
+#pragma unroll
+    for (int j = 0; j < s; ++j) {
+      const float keep = hi ? v[j + s] : v[j];
+      const float send = hi ? v[j] : v[j + s];
+      v[j] = keep + __shfl_xor(send, s, 64);
+    }
+  }
+  const int r = lane / kFinalCout, o = lane % kFinalCout, t = t0 + r;
+  if (lane >= NV || t >= tend || o >= cout) return;
+  const float vel = v[0] + (video ? a.bv : a.ba)[o];
+  const int traj = a.Nv * a.Cv + a.Na * a.A;
+  const size_t idx = (size_t)b * traj + (video ? (size_t)t * a.Cv + o
+                                               : (size_t)a.Nv * a.Cv + (size_t)(t - a.Nv) * a.A + o);
+  if (a.v_out) a.v_out[idx] = vel;
+  if (a.x) a.x[idx] += a.dsigma * vel;
+}
+
+// General form (any D % 64 == 0): four trajectory rows per wave; lane =
+// (row r = lane/16, output channel o = lane%16).  The 16 lanes of a row compute its LayerNorm statistics
 // together, stage the modulated row in LDS, then each lane forms one output
 // v[r][o] = u[r] . W^T[o] + b[o] (W^T packed [Cout][D], read through L1/L2),
 // stores the velocity and/or applies the Euler update x += dsigma v.
 constexpr int kFinalWaves = 1;
-__global__ __launch_bounds__(kFinalWaves * 64) void final_kernel(FinalArgs a) {
+__global__ __launch_bounds__(kFinalWaves * 64) void final_rows_kernel(FinalArgs a) {
   extern __shared__ float us[];  // [kFinalWaves * 4][D]
   const int nrow = a.Nv + a.Na;
   const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
@@ -555,12 +684,30 @@ hipError_t launch_ln_modulate(const float* h, const float* shift, const float* s
   return hipGetLastError();
 }
 
+template <int VEC, int R, int MAXC>
+void launch_final_t(const FinalArgs& a, hipStream_t s) {
+  const int waves = a.B * ((a.Nv + R - 1) / R + (a.Na + R - 1) / R);
+  if (waves > 0) launch_k(final_kernel<VEC, R, MAXC>, (waves + 3) / 4, 256, 0, s, a);
+}
+
 hipError_t launch_final(const FinalArgs& a, hipStream_t s) {
-  if (a.D % 4 || a.Cv > 16 || a.A > 16) return hipErrorInvalidValue;
-  const int rows = a.B * (a.Nv + a.Na);
-  const int per_block = kFinalWaves * 4;
-  const size_t lds = (size_t)per_block * a.D * sizeof(float);
-  launch_k(final_kernel, (rows + per_block - 1) / per_block, kFinalWaves * 64, lds, s, a);
+  if (a.D % kWave || a.D / kWave > kMaxVpl || a.Cv > kFinalCout || a.A > kFinalCout) return hipErrorInvalidValue;
+  // widest column vector D allows; rows per wave within the register budget
+  if (a.D % (4 * kWave) == 0) {
+    if (a.D <= 1536)
+      launch_final_t<4, 4, 6>(a, s);
+    else
+      launch_final_t<4, 2, 8>(a, s);
+  } else if (a.D % (2 * kWave) == 0 && a.D <= 1024) {
+    launch_final_t<2, 4, 8>(a, s);
+  } else if (a.D <= 1024) {
+    launch_final_t<1, 2, 16>(a, s);
+  } else {
+    const int rows = a.B * (a.Nv + a.Na);
+    const int per_block = kFinalWaves * 4;
+    const size_t lds = (size_t)per_block * a.D * sizeof(float);
+    launch_k(final_rows_kernel, (rows + per_block - 1) / per_block, kFinalWaves * 64, lds, s, a);
+  }
   return hipGetLastError();
 }
 

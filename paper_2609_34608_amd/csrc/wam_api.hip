@@ -181,7 +181,8 @@ WsLayout ws_layout(const Dims& d) {
   w.attn = take(MD * d.act);
   w.mlp = take((size_t)d.M * d.F * d.act);
   w.e = take(kTimeDim * 4); w.a1 = take(d.D * 4); w.sc = take(d.D * 4);
-  w.mod = take((size_t)d.Nmod * 4);
+  // modulation table of every schedule step (a pure function of sigma_k)
+  w.mod = take((size_t)WAM_MAX_STEPS * d.Nmod * 4);
   const size_t kmax = std::max(d.D, kTimeDim);
   const size_t nmax = std::max<size_t>(d.Nmod, d.D);
   w.gpart_floats = ((kmax + 31) / 32) * nmax;
@@ -231,6 +232,10 @@ struct wam_handle {
   std::vector<float> sigmas;
   int K = 0;
   bool layer_valid = false;
+  // modulation tables: slot k holds the table of sigma_k once computed; the
+  // step being enqueued reads slot mod_k
+  bool mod_valid[WAM_MAX_STEPS] = {};
+  int mod_k = 0;
   bool has_prev = false;
   int kappa = 0;
   double* host_stage = nullptr;  // pinned, small
@@ -274,6 +279,8 @@ int fail(wam_t h, int code, const std::string& msg) {
       return fail(h, WAM_E_HIP, std::string(#expr) + ": " + hipGetErrorString(e_));   \
   } while (0)
 
+float* mod_table(wam_t h) { return h->S(h->ws.mod) + (size_t)h->mod_k * h->d.Nmod; }
+
 // ---- per-launch timing for the measurement API
 struct ProfScope {
   wam_t h;
@@ -298,16 +305,23 @@ struct ProfScope {
 };
 
 // ---- step pieces
-int compute_conditioning(wam_t h, float sigma) {
+// Modulation table of schedule step k (timestep MLP, then every layer's adaLN
+// rows in one GEMV), computed on first use after the schedule is set and read
+// by the step's launches from then on; it depends only on sigma_k and the
+// weights.  Under capture the computation is recorded but not remembered.
+int compute_conditioning(wam_t h, int k) {
   const Dims& d = h->d;
   const DevLayout& wl = h->wl;
   const WsLayout& ws = h->ws;
   hipStream_t s = h->stream;
-  HIPCHK(h, launch_timestep_mlp(sigma, h->W(wl.t_w1), h->W(wl.t_b1), h->W(wl.t_w2), h->W(wl.t_b2), h->S(ws.a1),
-                                h->S(ws.sc), d.D, s));
+  h->mod_k = k;
+  if (h->mod_valid[k]) return WAM_OK;
+  HIPCHK(h, launch_timestep_mlp(h->sigmas[k], h->W(wl.t_w1), h->W(wl.t_b1), h->W(wl.t_w2), h->W(wl.t_b2),
+                                h->S(ws.a1), h->S(ws.sc), d.D, s));
   // sc now holds SiLU(c); all adaLN modulations in one pass
-  HIPCHK(h, launch_gemv(h->S(ws.sc), h->W<char>(wl.wmod), d.bf, h->W(wl.bmod), h->S(ws.mod),
+  HIPCHK(h, launch_gemv(h->S(ws.sc), h->W<char>(wl.wmod), d.bf, h->W(wl.bmod), mod_table(h),
                         h->S(ws.gpart), d.D, d.Nmod, 0, 0, s));
+  if (!h->capturing) h->mod_valid[k] = true;
   return WAM_OK;
 }
 
@@ -331,7 +345,7 @@ int run_layer(wam_t h, int l, const int* skip = nullptr) {
   const WsLayout& ws = h->ws;
   hipStream_t s = h->stream;
   const size_t D = d.D;
-  const float* mod = h->S(ws.mod) + (size_t)l * 6 * D;
+  const float* mod = mod_table(h) + (size_t)l * 6 * D;
   const float* lb = h->W(wl.lbias0 + wl.lbias_stride * l);
   const float* qkv_b = lb;
   const float* proj_b = lb + 3 * D;
@@ -433,7 +447,7 @@ RRRows rr_rows(const Dims& d, const wam_rr_profile* rr) {
 int final_step(wam_t h, int k, float* v_out, float* x_euler) {
   const Dims& d = h->d;
   FinalArgs f{};
-  const float* fm = h->S(h->ws.mod) + (size_t)d.L * 6 * d.D;
+  const float* fm = mod_table(h) + (size_t)d.L * 6 * d.D;
   f.h = h->S(h->ws.h); f.shift = fm; f.scale = fm + d.D;
   f.wv = h->W(h->wl.out_wvT); f.bv = h->W(h->wl.out_bv);
   f.wa = h->W(h->wl.out_waT); f.ba = h->W(h->wl.out_ba);
@@ -454,7 +468,7 @@ int enqueue_step_device(wam_t h, int k, const float* x, const float* cond, float
   const Dims& d = h->d;
   const WsLayout& ws = h->ws;
   hipStream_t s = h->stream;
-  int st = compute_conditioning(h, h->sigmas[k]);
+  int st = compute_conditioning(h, k);
   if (st) return st;
   if ((st = embed(h, x, cond))) return st;
   float* hh = h->S(ws.h);
@@ -524,6 +538,9 @@ int device_step(wam_t h, int k, const float* x, const float* cond, float* x_eule
   const size_t idx = (size_t)k * 3 + variant;
   if (h->graphs.size() < (size_t)h->K * 3) h->graphs.resize((size_t)h->K * 3, nullptr);
   if (!h->graphs[idx]) {
+    // the modulation table is computed outside the graph, which only reads it
+    int st0 = compute_conditioning(h, k);
+    if (st0) return st0;
     hipGraph_t g = nullptr;
     HIPCHK(h, hipStreamBeginCapture(h->stream, hipStreamCaptureModeThreadLocal));
     h->capturing = true;
@@ -568,7 +585,7 @@ int forward(wam_t h, int k, const float* x, const float* cond, float* v_out, flo
     if (active) h->layer_valid = true;  // either path leaves a valid retained state
     return WAM_OK;
   }
-  int st = compute_conditioning(h, h->sigmas[k]);
+  int st = compute_conditioning(h, k);
   if (st) return st;
   if ((st = embed(h, x, cond))) return st;
   float* hh = h->S(ws.h);
@@ -877,6 +894,7 @@ int wam_set_schedule(wam_t h, const float* sigmas, int K) {
     if (!(sigmas[i + 1] < sigmas[i])) return fail(h, WAM_E_ARG, "sigmas must decrease strictly");
   h->sigmas.assign(sigmas, sigmas + K + 1);
   h->K = K;
+  for (bool& v : h->mod_valid) v = false;
   drop_graphs(h);  // captured steps bake the noise levels in
   return WAM_OK;
 }
@@ -914,7 +932,7 @@ int wam_hidden(wam_t h, int k, const float* x, const float* cond, int n_layers, 
   int st = check_step(h, k, x, cond);
   if (st) return st;
   if (!h_out || n_layers < 0 || n_layers > h->d.L) return fail(h, WAM_E_ARG, "need 0 <= n_layers <= L");
-  if ((st = compute_conditioning(h, h->sigmas[k]))) return st;
+  if ((st = compute_conditioning(h, k))) return st;
   if ((st = embed(h, x, cond))) return st;
   if ((st = run_layers(h, 0, n_layers))) return st;
   HIPCHK(h, hipMemcpyAsync(h_out, h->S(h->ws.h), (size_t)h->d.M * h->d.D * 4, hipMemcpyDeviceToDevice, h->stream));

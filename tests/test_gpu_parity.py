@@ -56,6 +56,25 @@ def test_tiny_velocity_each_step(dev):
         assert rel_err(v.cpu().numpy(), ref) <= FP32_TOL, k
 
 
+@pytest.mark.parametrize("D,H", [(192, 3), (1088, 17), (2048, 32)])
+def test_hidden_sizes_velocity(dev, D, H):
+    """Velocity within 1e-4 at hidden sizes that select each form of the
+    final-layer kernel (8-byte columns up to 1024 wide, the general
+    per-row form, two rows per wave at 2048), on the tiny token layout."""
+    from paper_2609_34608_amd import runtime as R
+    spec = get_workload("tiny").replace(D=D, H=H, L=1)
+    W = make_weights(spec, bias_std=0.02)
+    m = R.WamModel(R.config_of(spec), W, device=dev)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    v, _ = m.velocity(1, to_dev(x0, dev), to_dev(cond, dev))
+    ref = OD.velocity(W, spec, x0, cond, sig[1])
+    assert rel_err(v.cpu().numpy(), ref) <= FP32_TOL
+    m.close()
+
+
 def test_tiny_native_chunk_and_capture(dev):
     spec, W, m, sig = _tiny(dev)
     x0 = make_initial_noise(spec)
