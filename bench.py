@@ -28,6 +28,7 @@ sys.path.insert(0, ROOT)
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
 HBM_PEAK_GBS = 8000.0
+ATTN_VARIANTS = {"auto": 0, "running": 1, "bounded": 2, "pingpong": 3}
 CLASS_NAMES = ["gemm_qkv", "gemm_proj", "gemm_fc1", "gemm_fc2", "attention", "rr_gate", "rr_inject",
                "rr_refresh"]
 
@@ -54,7 +55,7 @@ def kernel_class(name: str):
     m = re.search(r"gemm_splitk_reduce_kernel<\s*\d+,\s*(\d+)>", name)  # second pass of a split GEMM
     if m:
         return CLASS_NAMES[int(m.group(1))]
-    for key, cls in (("attn_bf16_kernel", "attention"), ("rr_row_sums_kernel", "rr_gate"),
+    for key, cls in (("attn_bf16", "attention"), ("rr_row_sums_kernel", "rr_gate"),
                      ("rr_finish_kernel", "rr_gate"), ("rr_inject_kernel", "rr_inject"),
                      ("rr_refresh_kernel", "rr_refresh")):
         if key in name:
@@ -126,6 +127,9 @@ def parse():
                    help="residual-rescaling mode of the timed replans")
     p.add_argument("--exec", default="host", choices=["host", "device", "graph"],
                    help="RR decision on the host, on the device, or on the device with graph replay")
+    p.add_argument("--attention", default="auto", choices=["auto", "running", "bounded", "pingpong"],
+                   help="bf16 attention kernel: auto, running-max softmax, bounded (fixed reference from the "
+                        "QK-norm score bound), or the bounded ping-pong form")
     p.add_argument("--copy-probe-mib", type=int, default=0,
                    help="one plain device copy of this size before timing (PMC calibration)")
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -172,6 +176,7 @@ def main():
     dev = torch.device("cuda:0")
     W = make_weights(spec)
     m = R.WamModel(R.config_of(spec), W, device=dev, own_stream=args.exec == "graph")
+    m.set_option(L.WAM_OPT_ATTENTION, ATTN_VARIANTS[args.attention])
     if args.exec in ("device", "graph"):
         m.set_option(L.WAM_OPT_DEVICE_DECISION, 1)
     if args.exec == "graph":
@@ -279,6 +284,7 @@ def main():
                          f"b0={spec.tr_b0} k1={spec.or_k1} shift={spec.shift_action}"),
             "step": "one replan (control step)",
             "exec": args.exec,
+            "attention": args.attention,
         },
         "action_chunks_per_s": round(chunks_per_s, 3),
         "denoise_steps_per_replan": n_steps / args.steps,
@@ -366,6 +372,7 @@ def idm_main(args):
     mv, ma = models
     K = sv.K
     for m in models:
+        m.set_option(L.WAM_OPT_ATTENTION, ATTN_VARIANTS[args.attention])
         m.set_option(L.WAM_OPT_DEVICE_DECISION, int(args.exec in ("device", "graph")))
         m.set_option(L.WAM_OPT_GRAPHS, int(args.exec == "graph"))
         m.set_schedule(1.0 - np.arange(K + 1, dtype=np.float64) / K)
@@ -466,6 +473,7 @@ def idm_main(args):
                          "single-branch RR per model"),
             "step": "one control step of the pair (video replan, then action replan)",
             "exec": args.exec,
+            "attention": args.attention,
         },
         "action_chunks_per_s": round(args.steps / elapsed, 3),
         "denoise_steps_per_replan": {"video": steps_v / args.steps, "action": steps_a / args.steps},

@@ -96,6 +96,17 @@ extern "C" {
                                      (stage, RR variant); needs the device decision
                                      and a non-default stream; graphs are re-captured
                                      when the schedule or the RR profile changes */
+#define WAM_OPT_ATTENTION 3       /* bf16 attention kernel (WAM_ATTN_*); every form
+                                     gives the same result up to rounding */
+#define WAM_ATTN_AUTO 0           /* default: a bounded form where the layer allows
+                                     it (ping-pong for long sequences), else the
+                                     running max */
+#define WAM_ATTN_RUNNING_MAX 1    /* online softmax with a running maximum          */
+#define WAM_ATTN_BOUNDED 2        /* QK-norm bounds every score by mref <= 60 (log2
+                                     units, from the gains): mref is the fixed
+                                     softmax reference, no running max             */
+#define WAM_ATTN_PINGPONG 3       /* bounded, 8 waves in two groups that alternate
+                                     MFMA and exp2 phases on each SIMD            */
 
 #define WAM_MAX_BATCH 16
 #define WAM_MAX_COMPONENTS 8

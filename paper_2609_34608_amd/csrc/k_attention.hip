@@ -78,6 +78,10 @@ __global__ __launch_bounds__(256) void qkv_relayout_kernel(RelayoutArgs a) {
 // ------------------------------------------------------------- bf16 flash attention
 constexpr int kDh = 64;
 constexpr int kKB = 64;  // keys per tile
+// largest fixed softmax reference: p >= 2^(-2 mref) must stay a normal float
+constexpr float kMaxBoundedRef = 60.0f;
+// launch_attention_cfg's wave-count value that selects the ping-pong kernel
+constexpr int kPingPong = 88;
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void global_void;
@@ -295,6 +299,406 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   }
 }
 
+// ------------------------------------------------------------- bf16 attention, bounded scores
+// When every score of the layer is known to lie in [-mref, mref] (QK-norm on:
+// |q.k| <= |q| |k| is fixed by the head size and the gains), the softmax
+// reference is the constant mref instead of a running max: softmax does not
+// depend on the reference, p = 2^(s - mref) stays in [2^-2mref, 1], and the
+// loop carries no max, no cross-lane step and no rescale.  The loop is also
+// software-pipelined: the S^T MFMAs of key tile j+1 are issued before the
+// exp2 of tile j, so the matrix cores work on the next tile while the VALU
+// turns the current one into P.  Stage slots: tile t sits in slot t % ST;
+// iteration j reads tiles j (V^T) and j+1 (K) and refills the slot of tile
+// j-1, so ST >= 3 and ST-3 tiles stay in flight across the barrier.
+template <int QT, int NW, int ST>
+__global__ __launch_bounds__(NW * 64) void attn_bf16_bounded_kernel(AttnArgs a) {
+  constexpr int QB = NW * QT * 16;
+  constexpr int NI = 16;
+  constexpr int IPW = NI / NW;
+  constexpr int U = ST % 2 == 0 ? ST : 2 * ST;  // unroll: slot and S buffer indices both static
+  static_assert(IPW >= 1 && IPW * NW == NI, "stage load split");
+  static_assert(ST >= 3 && (ST - 2) * IPW < 64, "stage count");
+  if (a.skip && *a.skip) return;
+  __shared__ __attribute__((aligned(1024))) bf16 sm[ST][128 * kDh];
+
+  const int bh = blockIdx.y;
+  const int b = bh / a.H, h = bh % a.H;
+  const int tid = threadIdx.x, lane = tid % 64, wid = tid / 64;
+  const int q0 = blockIdx.x * QB + wid * QT * 16;
+  const int g = lane / 16, lr = lane % 16;
+
+  const bf16* Q = static_cast<const bf16*>(a.q) + (size_t)bh * a.Tpad * kDh;
+  const bf16* Kg = static_cast<const bf16*>(a.k) + (size_t)bh * a.Tpad * kDh;
+  const bf16* Vg = static_cast<const bf16*>(a.vt) + (size_t)bh * kDh * a.Tpad;
+
+  bf16x8 qf[QT][2];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int q = q0 + qt * 16 + lr;
+      qf[qt][c] = q < a.Tpad ? *reinterpret_cast<const bf16x8*>(Q + (size_t)q * kDh + c * 32 + g * 8)
+                             : bf16x8{};
+    }
+
+  f32x4 o[4][QT];
+  f32x4 l[QT];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+#pragma unroll
+    for (int d = 0; d < 4; ++d) o[d][qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    l[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  bf16x8 ones;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ones[i] = static_cast<bf16>(1.0f);
+  const float nm = -a.mref;
+
+  // load instruction j of this wave: stage rows 8*(wid + NW*j) .. +7, as in
+  // the running-max kernel
+  const bf16* src[IPW];
+#pragma unroll
+  for (int j = 0; j < IPW; ++j) {
+    const int row = 8 * (wid + NW * j) + lane / 8;
+    const int col = ((lane % 8) ^ (row & 7)) * 8;
+    src[j] = j < IPW / 2 ? Kg + (size_t)row * kDh + col : Vg + (size_t)(row - 64) * a.Tpad + col;
+  }
+  auto issue = [&](auto S, int kb) __attribute__((always_inline)) {
+    constexpr int s = decltype(S)::value;
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      const size_t step = j < IPW / 2 ? (size_t)kKB * kDh : (size_t)kKB;
+      __builtin_amdgcn_global_load_lds((const global_void*)(src[j] + kb * step),
+                                       (lds_void*)(&sm[s][(wid + NW * j) * 512]), 16, 0, 0);
+    }
+  };
+
+  const int sw = lr & 7;
+  f32x4 sc[2][4][QT];  // S^T - mref of two key tiles: tile t in sc[t % 2]
+  auto qk = [&](auto S, auto BUF) __attribute__((always_inline)) {
+    const bf16* st = sm[decltype(S)::value];
+    constexpr int bi = decltype(BUF)::value;
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt) {
+      const bf16* krow = st + (kt * 16 + lr) * kDh;
+      const bf16x8 k0f = *reinterpret_cast<const bf16x8*>(krow + ((g ^ sw) * 8));
+      const bf16x8 k1f = *reinterpret_cast<const bf16x8*>(krow + (((g + 4) ^ sw) * 8));
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+        f32x4 z = {nm, nm, nm, nm};
+        z = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0f, qf[qt][0], z, 0, 0, 0);
+        sc[bi][kt][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1f, qf[qt][1], z, 0, 0, 0);
+      }
+    }
+  };
+  auto pv = [&](auto S, auto BUF, int k0, auto MASK) __attribute__((always_inline)) {
+    const bf16* st = sm[decltype(S)::value];
+    constexpr int bi = decltype(BUF)::value;
+    if constexpr (decltype(MASK)::value) {
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool live = k0 + kt * 16 + g * 4 + r < a.T;
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) sc[bi][kt][qt][r] = live ? sc[bi][kt][qt][r] : -INFINITY;
+        }
+    }
+    bf16x8 vf[4][2];
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        vf[d][c] = *reinterpret_cast<const bf16x8*>(st + (64 + d * 16 + lr) * kDh + (((4 * c + g) ^ sw) * 8));
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) {
+      bf16x8 pf[2];
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          pf[c][r] = static_cast<bf16>(__builtin_amdgcn_exp2f(sc[bi][2 * c][qt][r]));
+          pf[c][4 + r] = static_cast<bf16>(__builtin_amdgcn_exp2f(sc[bi][2 * c + 1][qt][r]));
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        l[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[c], l[qt], 0, 0, 0);
+#pragma unroll
+        for (int d = 0; d < 4; ++d) o[d][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[d][c], pf[c], o[d][qt], 0, 0, 0);
+      }
+    }
+  };
+
+  const int nkb = a.Tpad / kKB;
+  const std::integral_constant<bool, false> nomask{};
+  const std::integral_constant<bool, true> withmask{};
+  // prologue: tiles 0 .. ST-2 in flight, wait for tile 0, S of tile 0
+  static_for<ST - 1>([&](auto P) __attribute__((always_inline)) { issue(P, min((int)decltype(P)::value, nkb - 1)); });
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0((ST - 2) * IPW));
+  compiler_fence();
+  __builtin_amdgcn_s_barrier();
+  compiler_fence();
+  qk(std::integral_constant<int, 0>{}, std::integral_constant<int, 0>{});
+
+  // iteration kb < nkb-1: tile kb+1 has landed everywhere and tile kb-1's slot
+  // is free after the barrier; S of tile kb+1, then P and O of tile kb.  Past
+  // the end the refill repeats the last tile into dead slots (uniform counts).
+  auto body = [&](auto J, int kb) __attribute__((always_inline)) {
+    constexpr int j = decltype(J)::value;
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0((ST - 3) * IPW));
+    compiler_fence();
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+    issue(std::integral_constant<int, (j + ST - 1) % ST>{}, min(kb + ST - 1, nkb - 1));
+    qk(std::integral_constant<int, (j + 1) % ST>{}, std::integral_constant<int, (j + 1) % 2>{});
+    pv(std::integral_constant<int, j % ST>{}, std::integral_constant<int, j % 2>{}, kb * kKB, nomask);
+  };
+  // the last tile: its S and its V^T stage are already resident
+  auto last = [&](auto J, int kb) __attribute__((always_inline)) {
+    constexpr int j = decltype(J)::value;
+    pv(std::integral_constant<int, j % ST>{}, std::integral_constant<int, j % 2>{}, kb * kKB, withmask);
+  };
+  const int nbody = nkb - 1;
+  int kb0 = 0;
+  for (; kb0 + U <= nbody; kb0 += U)
+    static_for<U>([&](auto J) __attribute__((always_inline)) { body(J, kb0 + decltype(J)::value); });
+  static_for<U>([&](auto J) __attribute__((always_inline)) {
+    const int kb = kb0 + decltype(J)::value;
+    if (kb < nbody) body(J, kb);
+    else if (kb == nbody) last(J, kb);
+  });
+  __builtin_amdgcn_s_waitcnt(0);
+
+  bf16* out = static_cast<bf16*>(a.out);
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    const float inv = 1.0f / l[qt][0];
+    const int q = q0 + qt * 16 + lr;
+    if (q >= a.T) continue;
+    bf16* orow = out + ((size_t)b * a.T + q) * a.D + h * kDh;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      bf16x4 v;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v[r] = static_cast<bf16>(o[d][qt][r] * inv);
+      *reinterpret_cast<bf16x4*>(orow + d * 16 + g * 4) = v;
+    }
+  }
+}
+
+// ------------------------------------------------------------- bf16 attention, bounded scores, ping-pong
+// Same fixed-reference softmax as above, with the work of a key tile split
+// into a matrix phase M(t) (S^T of tile t, then O += V^T P^T of tile t-1)
+// and a vector phase V(t) (P of tile t = exp2 of S, packed to bf16).  The 8
+// waves form two groups that share the block's K / V^T stages and run half a
+// phase apart: waves w and w+4 sit on the same SIMD, and while one runs its
+// MFMAs the other runs its exp2s, so the two pipes overlap instead of taking
+// turns inside one wave.  Every phase ends at a block barrier: with intervals
+// counted from 0, group 0 runs M(t) in interval 2t and V(t) in 2t+1, group 1
+// runs M(t) in 2t+1 and V(t) in 2t+2.  Tile t is read in intervals 2t .. 2t+3
+// (its K by both groups' M(t), its V^T by both groups' M(t+1)); the barrier
+// that opens interval 2m checks that tile m has landed and refills the slot
+// of tile m-2 with tile m+ST-2.
+template <int QT, int ST>
+__global__ __launch_bounds__(512) void attn_bf16_pingpong_kernel(AttnArgs a) {
+  constexpr int NW = 8;
+  constexpr int QB = NW * QT * 16;
+  constexpr int NI = 16;
+  constexpr int IPW = NI / NW;
+  static_assert(ST >= 4 && (ST - 1) * IPW < 64, "stage count");
+  if (a.skip && *a.skip) return;
+  __shared__ __attribute__((aligned(1024))) bf16 sm[ST][128 * kDh];
+
+  const int bh = blockIdx.y;
+  const int b = bh / a.H, h = bh % a.H;
+  const int tid = threadIdx.x, lane = tid % 64, wid = tid / 64;
+  const bool grp1 = wid >= 4;
+  const int q0 = blockIdx.x * QB + wid * QT * 16;
+  const int g = lane / 16, lr = lane % 16;
+
+  const bf16* Q = static_cast<const bf16*>(a.q) + (size_t)bh * a.Tpad * kDh;
+  const bf16* Kg = static_cast<const bf16*>(a.k) + (size_t)bh * a.Tpad * kDh;
+  const bf16* Vg = static_cast<const bf16*>(a.vt) + (size_t)bh * kDh * a.Tpad;
+
+  bf16x8 qf[QT][2];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int q = q0 + qt * 16 + lr;
+      qf[qt][c] = q < a.Tpad ? *reinterpret_cast<const bf16x8*>(Q + (size_t)q * kDh + c * 32 + g * 8)
+                             : bf16x8{};
+    }
+  f32x4 o[4][QT];
+  f32x4 l[QT];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+#pragma unroll
+    for (int d = 0; d < 4; ++d) o[d][qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    l[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  bf16x8 ones;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ones[i] = static_cast<bf16>(1.0f);
+  const float nm = -a.mref;
+
+  const bf16* src[IPW];
+#pragma unroll
+  for (int j = 0; j < IPW; ++j) {
+    const int row = 8 * (wid + NW * j) + lane / 8;
+    const int col = ((lane % 8) ^ (row & 7)) * 8;
+    src[j] = j < IPW / 2 ? Kg + (size_t)row * kDh + col : Vg + (size_t)(row - 64) * a.Tpad + col;
+  }
+  const int nkb = a.Tpad / kKB;
+  auto issue = [&](int t) __attribute__((always_inline)) {
+    const int slot = t % ST, kb = min(t, nkb - 1);
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+      const size_t step = j < IPW / 2 ? (size_t)kKB * kDh : (size_t)kKB;
+      __builtin_amdgcn_global_load_lds((const global_void*)(src[j] + kb * step),
+                                       (lds_void*)(&sm[slot][(wid + NW * j) * 512]), 16, 0, 0);
+    }
+  };
+  // Barriers.  The scheduling barriers keep each phase's instructions between
+  // its two block barriers (the compiler would otherwise merge the phases).
+  // Barrier opening interval 2m: tile m has landed (every wave's part of it),
+  // then the slot of tile m-2 takes tile m+ST-2 (at m = 1 that reloads tile
+  // ST-1 into its own unread slot; tiles past the end repeat the last one
+  // into dead slots), which keeps the wait counts uniform and the loop free
+  // of branches.
+  auto sync_even = [&](int m) __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0((ST - 3) * IPW));
+    compiler_fence();
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    compiler_fence();
+    issue(m + ST - 2);
+  };
+  auto sync_odd = [&]() __attribute__((always_inline)) {
+    compiler_fence();
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    compiler_fence();
+  };
+
+  const int sw = lr & 7;
+  f32x4 sc[4][QT];
+  bf16x8 pf[QT][2];
+  // M(t): S^T of tile t (QK) and O += V^T P^T of tile t-1 (PV)
+  auto mphase = [&](int t, auto QK, auto PV) __attribute__((always_inline)) {
+    if constexpr (decltype(QK)::value) {
+      const bf16* st = sm[t % ST];
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) {
+        const bf16* krow = st + (kt * 16 + lr) * kDh;
+        const bf16x8 k0f = *reinterpret_cast<const bf16x8*>(krow + ((g ^ sw) * 8));
+        const bf16x8 k1f = *reinterpret_cast<const bf16x8*>(krow + (((g + 4) ^ sw) * 8));
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) {
+          f32x4 z = {nm, nm, nm, nm};
+          z = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0f, qf[qt][0], z, 0, 0, 0);
+          sc[kt][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1f, qf[qt][1], z, 0, 0, 0);
+        }
+      }
+    }
+    if constexpr (decltype(PV)::value) {
+      const bf16* st = sm[(t - 1) % ST];
+      bf16x8 vf[4][2];
+#pragma unroll
+      for (int d = 0; d < 4; ++d)
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+          vf[d][c] = *reinterpret_cast<const bf16x8*>(st + (64 + d * 16 + lr) * kDh + (((4 * c + g) ^ sw) * 8));
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          l[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[qt][c], l[qt], 0, 0, 0);
+#pragma unroll
+          for (int d = 0; d < 4; ++d)
+            o[d][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[d][c], pf[qt][c], o[d][qt], 0, 0, 0);
+        }
+    }
+  };
+  // V(t): P of tile t; the last tile masks keys >= T
+  auto vphase = [&](int t, auto MASK) __attribute__((always_inline)) {
+    if constexpr (decltype(MASK)::value) {
+      const int k0 = t * kKB;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const bool live = k0 + kt * 16 + g * 4 + r < a.T;
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) sc[kt][qt][r] = live ? sc[kt][qt][r] : -INFINITY;
+        }
+    }
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          pf[qt][c][r] = static_cast<bf16>(__builtin_amdgcn_exp2f(sc[2 * c][qt][r]));
+          pf[qt][c][4 + r] = static_cast<bf16>(__builtin_amdgcn_exp2f(sc[2 * c + 1][qt][r]));
+        }
+  };
+  const std::integral_constant<bool, false> no{};
+  const std::integral_constant<bool, true> yes{};
+
+  static_for<ST>([&](auto P) __attribute__((always_inline)) { issue(decltype(P)::value); });
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0((ST - 1) * IPW));
+  sync_odd();  // opens interval 0: tile 0 has landed everywhere
+  // one straight-line program per group (no branch between the barriers)
+  if (!grp1) {
+    mphase(0, yes, no);
+    sync_odd();
+    for (int t = 1; t < nkb; ++t) {
+      vphase(t - 1, no);
+      sync_even(t);
+      mphase(t, yes, yes);
+      sync_odd();
+    }
+    vphase(nkb - 1, yes);
+    sync_even(nkb);
+    mphase(nkb, no, yes);
+    sync_odd();  // both groups pass the same number of barriers
+  } else {
+    sync_odd();  // group 1 starts one interval later
+    mphase(0, yes, no);
+    sync_even(1);
+    for (int t = 1; t < nkb; ++t) {
+      vphase(t - 1, no);
+      sync_odd();
+      mphase(t, yes, yes);
+      sync_even(t + 1);
+    }
+    vphase(nkb - 1, yes);
+    sync_odd();
+    mphase(nkb, no, yes);
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+
+  bf16* out = static_cast<bf16*>(a.out);
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    const float inv = 1.0f / l[qt][0];
+    const int q = q0 + qt * 16 + lr;
+    if (q >= a.T) continue;
+    bf16* orow = out + ((size_t)b * a.T + q) * a.D + h * kDh;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      bf16x4 v;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) v[r] = static_cast<bf16>(o[d][qt][r] * inv);
+      *reinterpret_cast<bf16x4*>(orow + d * 16 + g * 4) = v;
+    }
+  }
+}
+
 // ------------------------------------------------------------- fp32 attention
 // One thread per query, online softmax over all keys (parity mode only).
 template <int DH>
@@ -352,12 +756,31 @@ hipError_t launch_qkv_relayout(const RelayoutArgs& a, bool bf16_mode, hipStream_
 // grid for qt query tiles per wave and nw waves per block
 // (qt, nw, st): query tiles of 16 per wave, waves per block, LDS stages of
 // one 64-key K / V^T tile.  Only the instantiated combinations are accepted.
-hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int st, hipStream_t s) {
+hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int st, hipStream_t s, bool bounded) {
   // every key tile but the last is fully inside [0, T), the last holds >= 1 key
   if (a.dh != kDh || a.T <= 0 || a.Tpad % kKB || a.T > a.Tpad || a.T <= a.Tpad - kKB) return hipErrorInvalidValue;
-  const int qb = qt * nw * 16;
+  const int qb = qt * (nw == kPingPong ? 8 : nw) * 16;
   const dim3 grid((a.T + qb - 1) / qb, a.B * a.H);
   const int key = qt * 10000 + nw * 100 + st;
+  if (bounded) {
+    if (!a.bounded || !(a.mref >= 0.f && a.mref <= kMaxBoundedRef)) return hipErrorInvalidValue;
+    switch (key) {
+      case 10404: launch_k(attn_bf16_bounded_kernel<1, 4, 4>, grid, 256, 0, s, a); break;
+      case 20404: launch_k(attn_bf16_bounded_kernel<2, 4, 4>, grid, 256, 0, s, a); break;
+      case 20403: launch_k(attn_bf16_bounded_kernel<2, 4, 3>, grid, 256, 0, s, a); break;
+      case 10204: launch_k(attn_bf16_bounded_kernel<1, 2, 4>, grid, 128, 0, s, a); break;
+      case 20804: launch_k(attn_bf16_bounded_kernel<2, 8, 4>, grid, 512, 0, s, a); break;
+      case 40404: launch_k(attn_bf16_bounded_kernel<4, 4, 4>, grid, 256, 0, s, a); break;
+      // ping-pong kernel: nw = kPingPong (8 waves in two groups)
+      case 28804: launch_k(attn_bf16_pingpong_kernel<2, 4>, grid, 512, 0, s, a); break;
+      case 28805: launch_k(attn_bf16_pingpong_kernel<2, 5>, grid, 512, 0, s, a); break;
+      case 18804: launch_k(attn_bf16_pingpong_kernel<1, 4>, grid, 512, 0, s, a); break;
+      case 48804: launch_k(attn_bf16_pingpong_kernel<4, 4>, grid, 512, 0, s, a); break;
+      case 38804: launch_k(attn_bf16_pingpong_kernel<3, 4>, grid, 512, 0, s, a); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   switch (key) {
     case 10404: launch_k(attn_bf16_kernel<1, 4, 4>, grid, 256, 0, s, a); break;
     case 20404: launch_k(attn_bf16_kernel<2, 4, 4>, grid, 256, 0, s, a); break;
@@ -372,7 +795,29 @@ hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int st, hipSt
   return hipGetLastError();
 }
 
+float attention_score_bound(const float* q_g, const float* k_g) {
+  // q = log2(e)/8 * g_q (.) qhat and k = g_k (.) khat with |qhat|, |khat| <= 8
+  // (unit RMS over 64 dims), so |q.k| <= log2(e)/8 * 64 * max|g_q| * max|g_k|;
+  // bf16 rounding of each element adds at most 2^-8 relative per operand
+  float gq = 0.f, gk = 0.f;
+  for (int i = 0; i < kDh; ++i) {
+    gq = fmaxf(gq, fabsf(q_g[i]));
+    gk = fmaxf(gk, fabsf(k_g[i]));
+  }
+  return kQLog2Scale * 64.0f * gq * gk * (1.0f + 1.0f / 128.0f) + 1e-3f;
+}
+
 hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s) {
+  if (bf16_mode && a.bounded && a.variant != WAM_ATTN_RUNNING_MAX) {
+    // ping-pong (512 queries per block) for long sequences that still give
+    // about two blocks per CU; otherwise 128 or 64 queries per block
+    const long bpp = (long)((a.T + 511) / 512) * a.B * a.H;
+    if (a.variant == WAM_ATTN_PINGPONG || (a.variant == WAM_ATTN_AUTO && a.T >= 4096 && bpp >= 384))
+      return launch_attention_cfg(a, 4, kPingPong, 4, s, true);
+    const long blocks = (long)((a.T + 127) / 128) * a.B * a.H;
+    if (blocks >= 256) return launch_attention_cfg(a, 2, 4, 4, s, true);
+    return launch_attention_cfg(a, 1, 4, 4, s, true);
+  }
   if (bf16_mode) {
     // 4 waves x 32 queries (two K/V stages) when that fills the chip, else
     // 4 waves x 16 queries

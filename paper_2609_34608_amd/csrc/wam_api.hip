@@ -241,6 +241,10 @@ struct wam_handle {
   double* host_stage = nullptr;  // pinned, small
   std::string err;
   ProfSlot prof[WAM_KC_COUNT];
+  // per-layer fixed softmax reference (log2 units) of the bf16 attention, or
+  // -1 where the scores have no usable bound
+  std::vector<float> attn_mref;
+  int attn_variant = WAM_ATTN_AUTO;
   bool dev_decision = false;  // RR decision kept on the device (no host round trip per step)
   bool use_graphs = false;    // replay captured step graphs inside wam_replan
   bool capturing = false;
@@ -388,6 +392,9 @@ int run_layer(wam_t h, int l, const int* skip = nullptr) {
     ProfScope ps(h, WAM_KC_ATTENTION, 4.0 * d.B * (double)d.T * d.T * D);
     AttnArgs at{h->S<char>(ws.q), h->S<char>(ws.k), h->S<char>(ws.vt), h->S<char>(ws.attn),
                 d.B, d.H, d.T, d.Tpad, d.dh, d.D, skip};
+    at.mref = h->attn_mref[l];
+    at.bounded = d.bf && at.mref >= 0.f;
+    at.variant = h->attn_variant;
     HIPCHK(h, launch_attention(at, d.bf, s));
   }
   {
@@ -818,6 +825,12 @@ int wam_init(const wam_config* cfg, const float* hw, size_t n_hw, void* dev_weig
     memcpy(buf.data() + lb + (4 * D + F) * 4, L0 + hl.fc2_b, D * 4);
     memcpy(buf.data() + lb + (5 * D + F) * 4, L0 + hl.q_g, d.dh * 4);
     memcpy(buf.data() + lb + (5 * D + F + d.dh) * 4, L0 + hl.k_g, d.dh * 4);
+    float mref = -1.f;
+    if (d.bf && cfg->qk_norm) {
+      mref = attention_score_bound(L0 + hl.q_g, L0 + hl.k_g);
+      if (!(mref <= 60.0f)) mref = -1.f;
+    }
+    h->attn_mref.push_back(mref);
     const size_t lw = wl.lw0 + wl.lw_stride * l;
     put_T(lw, L0 + hl.qkv_w, D, 3 * D);
     put_T(lw + 3 * D * D * d.act, L0 + hl.proj_w, D, D);
@@ -881,6 +894,11 @@ int wam_set_option(wam_t h, int option, int value) {
       if (value && h->stream == nullptr) return fail(h, WAM_E_UNSUPPORTED, "graphs need a non-default stream");
       if (!value) drop_graphs(h);
       h->use_graphs = value != 0;
+      return WAM_OK;
+    case WAM_OPT_ATTENTION:
+      if (value < WAM_ATTN_AUTO || value > WAM_ATTN_PINGPONG) return fail(h, WAM_E_ARG, "unknown attention kernel");
+      if (value != h->attn_variant) drop_graphs(h);  // captured launches name the kernel
+      h->attn_variant = value;
       return WAM_OK;
     default:
       return fail(h, WAM_E_ARG, "unknown option");

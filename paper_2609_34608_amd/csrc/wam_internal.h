@@ -153,10 +153,21 @@ struct AttnArgs {
   void* out;       // [B*T][D], head h at columns h*dh
   int B, H, T, Tpad, dh, D;
   const int* skip; // device flag: when non-null and set, the launch does nothing
+  // bf16 mode: when bounded is set, every score (log2 units, as the QKV
+  // epilogue stores q) lies in [-mref, mref] and the kernel uses mref as its
+  // fixed softmax reference
+  float mref;
+  int bounded;
+  int variant;  // WAM_ATTN_*: AUTO picks by shape; bounded forms need bounded set
 };
 hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s);
-// bf16 kernel with qt query tiles of 16 per wave and nw waves per block
-hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int st, hipStream_t s);
+// bf16 kernel with qt query tiles of 16 per wave and nw waves per block;
+// bounded selects the fixed-reference kernels (needs a.bounded), nw = 88 the
+// ping-pong form (8 waves in two groups)
+hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int st, hipStream_t s, bool bounded = false);
+// Largest score magnitude, log2 units, that the bf16 QKV epilogue can produce
+// for head size 64 with QK-norm gains q_g, k_g (host arrays of 64)
+float attention_score_bound(const float* q_g, const float* k_g);
 
 // qkv [B*T][3D] -> q, k (optionally RMS-normalised with gains) and v^T
 struct RelayoutArgs {

@@ -1,0 +1,106 @@
+"""GPU parity of the bf16 attention kernels through the C ABI.
+
+Three kernels exist in bf16 mode: the online softmax with a running max, and
+(with QK-norm, when the gains bound every score) a fixed softmax reference
+equal to that bound, in a pipelined form and in a ping-pong form whose two
+wave groups alternate MFMA and exp2 phases.  Each must match the float64
+oracle at every sequence length class: one key tile, an exact multiple of
+the tile, a one-key tail, and several tiles with a ragged tail.  Tolerance:
+2e-2 (bf16 contractions), max |got-ref| / max |ref|.
+"""
+import numpy as np
+import pytest
+
+from oracle import dit as OD
+from synth import get_workload, make_weights, make_initial_noise, make_observations
+from gpu_common import device, to_dev, rel_err, f32_sigmas
+
+pytestmark = pytest.mark.gpu
+
+BF16_TOL = 2e-2
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return device()
+
+
+# (Nv, Na, No) -> T = 40 (one tile), 64 (exact), 65 (one-key tail), 200, 333
+_LENGTHS = [(24, 8, 8), (40, 16, 8), (41, 16, 8), (160, 32, 8), (288, 32, 13)]
+
+
+def _spec(Nv, Na, No, L=2):
+    return get_workload("small").replace(L=L, D=128, H=2, F=512, Nv=Nv, Na=Na, No=No, B=2)
+
+
+_VARIANTS = ["RUNNING_MAX", "BOUNDED", "PINGPONG"]
+
+
+@pytest.mark.parametrize("variant", _VARIANTS)
+@pytest.mark.parametrize("lengths", _LENGTHS)
+def test_bf16_attention_lengths_match_oracle(dev, lengths, variant):
+    from paper_2609_34608_amd import runtime as R, _lib as L
+    spec = _spec(*lengths)
+    W = make_weights(spec, bias_std=0.02, gain_std=0.1)
+    m = R.WamModel(R.config_of(spec), W, device=dev)
+    m.set_option(L.WAM_OPT_ATTENTION, getattr(L, "WAM_ATTN_" + variant))
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    for k in (0, 6):
+        v, _ = m.velocity(k, to_dev(x0, dev), to_dev(cond, dev))
+        ref = OD.velocity(W, spec, x0, cond, sig[k])
+        e = rel_err(v.cpu().numpy(), ref)
+        print(f"T={spec.T} {variant} step {k} velocity rel err {e:.3e}")
+        assert e <= BF16_TOL, (spec.T, k, e)
+    m.close()
+
+
+def test_attention_kernels_agree(dev):
+    """The kernels differ only in the bf16 rounding of P (and the bounded
+    forms not at all from each other): their layer updates agree far inside
+    the bf16 tolerance."""
+    from paper_2609_34608_amd import runtime as R, _lib as L
+    spec = _spec(288, 32, 13, L=1)
+    W = make_weights(spec, bias_std=0.02, gain_std=0.1)
+    m = R.WamModel(R.config_of(spec), W, device=dev)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    outs = {}
+    for v in _VARIANTS:
+        m.set_option(L.WAM_OPT_ATTENTION, getattr(L, "WAM_ATTN_" + v))
+        outs[v] = m.hidden(2, to_dev(x0, dev), to_dev(cond, dev), 1).cpu().numpy()
+    h0 = m.hidden(2, to_dev(x0, dev), to_dev(cond, dev), 0).cpu().numpy()
+    e = rel_err(outs["BOUNDED"] - h0, outs["RUNNING_MAX"] - h0)
+    print(f"bounded vs running-max layer update rel diff {e:.3e}")
+    assert e <= 5e-3
+    # the two bounded kernels sum the same bf16 P in the same MFMA order
+    np.testing.assert_array_equal(outs["BOUNDED"], outs["PINGPONG"])
+    m.close()
+
+
+def test_large_gains_fall_back_to_running_max(dev):
+    """Gains large enough that the score bound exceeds the fixed-reference
+    limit: the library takes the running-max kernel, even when a bounded
+    kernel is asked for, and still matches."""
+    from paper_2609_34608_amd import runtime as R, _lib as L
+    spec = _spec(160, 32, 8, L=1)
+    W = make_weights(spec, bias_std=0.02)
+    for l in range(spec.L):
+        W[f"l{l}.q_g"][:] = 2.5
+        W[f"l{l}.k_g"][:] = 2.2
+    m = R.WamModel(R.config_of(spec), W, device=dev)
+    m.set_option(L.WAM_OPT_ATTENTION, L.WAM_ATTN_PINGPONG)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    v, _ = m.velocity(3, to_dev(x0, dev), to_dev(cond, dev))
+    ref = OD.velocity(W, spec, x0, cond, sig[3])
+    e = rel_err(v.cpu().numpy(), ref)
+    print(f"gains 2.5 x 2.2 velocity rel err {e:.3e}")
+    assert e <= BF16_TOL
+    m.close()
