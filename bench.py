@@ -49,7 +49,7 @@ def traffic_path(workload: str) -> str:
 
 def kernel_class(name: str):
     """Kernel class of a rocprofv3 kernel name (None if not a timed class)."""
-    m = re.search(r"gemm_bf16_kernel<\s*\d+,\s*\d+,\s*\d+,\s*\d+,\s*\d+,\s*\d+,\s*(\d+),", name)
+    m = re.search(r"gemm_bf16_kernel<\s*\d+,\s*\d+,\s*\d+,\s*\d+,\s*\d+,\s*\d+,\s*\d+,\s*(\d+),", name)
     if m:
         return CLASS_NAMES[int(m.group(1))]
     m = re.search(r"gemm_splitk_reduce_kernel<\s*\d+,\s*(\d+)>", name)  # second pass of a split GEMM

@@ -8,14 +8,16 @@
 // columns of one row and the epilogue stores 8 (bf16) or 16 (fp32) contiguous
 // bytes.  A block of WGM x WGN waves owns a BM x BN tile.
 //
-// K advances 32 at a time through ST LDS stages.  Each stage holds BM
-// activation rows and BN weight rows of 64 bytes, filled straight from global
-// memory by global_load_lds_dwordx4 (16 bytes per lane, one 1 KiB run of LDS
-// per instruction, no register staging): ST-1 stages are in flight while one
-// is multiplied.  Inside a row the four 16-byte chunks are XOR-swizzled by
-// (row >> 1) & 3, which keeps the ds_read_b128 operand reads (16 rows x one
-// chunk per 16 lanes) free of bank conflicts; the loads pick their global
-// chunk so that the LDS image comes out swizzled.  The compiler cannot follow
+// K advances BK (32, 64 or 128) at a time through ST LDS stages.  Each stage
+// holds BM activation rows and BN weight rows of 2*BK bytes, filled straight
+// from global memory by global_load_lds_dwordx4 (16 bytes per lane, one 1 KiB
+// run of LDS per instruction, no register staging): ST-1 stages are in flight
+// while one is multiplied.  Inside a row the 16-byte chunks are XOR-swizzled
+// ((row >> 1) & 3 for 64-byte rows, row & 7 for longer ones), which keeps the
+// ds_read_b128 operand reads (16 rows x one chunk per 16 lanes) free of bank
+// conflicts; the loads pick their global chunk so that the LDS image comes out
+// swizzled.  A deeper stage gives each wave BK/32 MFMA k-steps per barrier,
+// which is what short tiles (small M) need.  The compiler cannot follow
 // the LDS writes of these loads, so the loop waits on vmcnt itself and uses a
 // bare s_barrier (a workgroup fence would drain every load in flight).
 // Blocks are renumbered so that each XCD (dispatch is round-robin over 8 XCDs)
@@ -30,7 +32,7 @@
 namespace wam {
 namespace gemm {
 
-constexpr int kBK = 32;    // K per stage: one 64-byte LDS row
+constexpr int kBK = 32;    // K per MFMA step (and the smallest stage depth)
 constexpr int kGroupM = 8;
 constexpr int kXcd = 8;
 
@@ -42,8 +44,12 @@ typedef __attribute__((address_space(1))) void global_void;
 // scalar-memory operation outstanding
 constexpr int waitcnt_vm_lgkm0(int n) { return (n & 0xf) | ((n >> 4) << 14) | (0x7 << 4); }
 
-// swizzled 16-byte chunk of a 64-byte LDS row
-__device__ __forceinline__ int chunk_swizzle(int row) { return (row >> 1) & 3; }
+// XOR swizzle of the 16-byte chunks of an LDS row of 2*BK bytes
+template <int BK>
+__device__ __forceinline__ int chunk_swizzle(int row) {
+  if constexpr (BK == 32) return (row >> 1) & 3;
+  else return row & 7;
+}
 
 // compiler-only memory barrier: keeps LDS and global accesses on their side
 __device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
@@ -201,21 +207,25 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const f32x4 (&acc)
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int ST, int EPI, int ROLE, bool SPLIT>
+template <int BM, int BN, int WGM, int WGN, int ST, int BK, int EPI, int ROLE, bool SPLIT>
 __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
   constexpr int NW = WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN;  // wave tile
   constexpr int TM = WM / 16, TN = WN / 16;
   constexpr int ROWS = BM + BN;                // LDS rows per stage: activations, then weights
-  constexpr int NI = ROWS / 16;                // 1 KiB load instructions per stage
+  constexpr int CPR = BK / 8;                  // 16-byte chunks per LDS row
+  constexpr int RPI = 64 / CPR;                // rows per 1 KiB load instruction
+  constexpr int NI = ROWS / RPI;               // load instructions per stage
   constexpr int IPW = NI / NW;                 // ... per wave
+  constexpr int KS = BK / kBK;                 // MFMA k-steps per stage
+  static_assert(BK == 32 || BK == 64 || BK == 128, "stage depth");
   static_assert(TM >= 1 && TN >= 1, "wave tile too small");
   static_assert(IPW >= 1 && IPW * NW == NI, "stage rows / wave mismatch");
   static_assert(EPI != EPI_QKV || WN % 64 == 0, "QKV epilogue needs whole heads per wave");
   static_assert(ST >= 2 && (ST - 2) * IPW < 64, "stage count");
   if (a.skip && *a.skip) return;
 
-  __shared__ __attribute__((aligned(1024))) bf16 sm[ST][ROWS * kBK];
+  __shared__ __attribute__((aligned(1024))) bf16 sm[ST][ROWS * BK];
 
   const int tiles_m = (a.M + BM - 1) / BM, tiles_n = a.N / BN;
   int tm, tn;
@@ -228,21 +238,21 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
   const int K = a.K;
   int kbeg = 0, kend = K;
   if constexpr (SPLIT) {
-    const int per = K / gridDim.z;  // host guarantees divisibility by kBK * splits
+    const int per = K / gridDim.z;  // host guarantees divisibility by BK * splits
     kbeg = blockIdx.z * per;
     kend = kbeg + per;
   }
-  const int nk = (kend - kbeg) / kBK;
+  const int nk = (kend - kbeg) / BK;
 
-  // Load instruction j of this wave fills LDS rows 16*(wid + NW*j) .. +15;
-  // lane l writes LDS chunk l%4 of row l/4, i.e. global chunk (l%4) ^ swizzle.
-  // Activation rows past M read row M-1 (their products reach only output
-  // rows that are never stored).
+  // Load instruction j of this wave fills LDS rows RPI*(wid + NW*j) .. +RPI-1;
+  // lane l writes LDS chunk l%CPR of row l/CPR, i.e. global chunk
+  // (l%CPR) ^ swizzle.  Activation rows past M read row M-1 (their products
+  // reach only output rows that are never stored).
   const bf16* src[IPW];
 #pragma unroll
   for (int j = 0; j < IPW; ++j) {
-    const int row = 16 * (wid + NW * j) + lane / 4;
-    const int col = ((lane % 4) ^ chunk_swizzle(row)) * 8;
+    const int row = RPI * (wid + NW * j) + lane / CPR;
+    const int col = ((lane % CPR) ^ chunk_swizzle<BK>(row)) * 8;
     src[j] = row < BM ? A + (size_t)min(m0 + row, a.M - 1) * K + kbeg + col
                       : W + (size_t)(n0 + row - BM) * K + kbeg + col;
   }
@@ -250,8 +260,8 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
     constexpr int s = decltype(S)::value;
 #pragma unroll
     for (int j = 0; j < IPW; ++j)
-      __builtin_amdgcn_global_load_lds((const global_void*)(src[j] + kt * kBK),
-                                       (lds_void*)(&sm[s][(wid + NW * j) * 16 * kBK]), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const global_void*)(src[j] + kt * BK),
+                                       (lds_void*)(&sm[s][(wid + NW * j) * RPI * BK]), 16, 0, 0);
   };
 
   f32x4 acc[TN][TM];
@@ -260,24 +270,29 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < TM; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // operand reads: lane (lr, lg) takes chunk lg of row lr of each 16-row tile
-  // (tile row offsets are multiples of 16, so the swizzle depends on lr only)
+  // operand reads: for k-step ks, lane (lr, lg) takes chunk 4*ks + lg of row
+  // lr of each 16-row tile (tile row offsets are multiples of 16, so the
+  // swizzle depends on lr only)
   const int lr = lane % 16, lg = lane / 16;
-  const int ch = (lg ^ chunk_swizzle(lr)) * 8;
-  const int aoff = (wm * WM + lr) * kBK + ch;
-  const int woff = (BM + wn * WN + lr) * kBK + ch;
+  const int sw = chunk_swizzle<BK>(lr);
+  const int arow = (wm * WM + lr) * BK;
+  const int wrow = (BM + wn * WN + lr) * BK;
   auto compute = [&](auto S) __attribute__((always_inline)) {
     constexpr int s = decltype(S)::value;
-    bf16x8 af[TM], wf[TN];
 #pragma unroll
-    for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const bf16x8*>(&sm[s][aoff + i * 16 * kBK]);
+    for (int ks = 0; ks < KS; ++ks) {
+      const int ch = ((4 * ks + lg) ^ sw) * 8;
+      bf16x8 af[TM], wf[TN];
 #pragma unroll
-    for (int j = 0; j < TN; ++j) wf[j] = *reinterpret_cast<const bf16x8*>(&sm[s][woff + j * 16 * kBK]);
+      for (int i = 0; i < TM; ++i) af[i] = *reinterpret_cast<const bf16x8*>(&sm[s][arow + ch + i * 16 * BK]);
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+      for (int j = 0; j < TN; ++j) wf[j] = *reinterpret_cast<const bf16x8*>(&sm[s][wrow + ch + j * 16 * BK]);
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-        acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j], af[i], acc[j][i], 0, 0, 0);
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j], af[i], acc[j][i], 0, 0, 0);
+    }
   };
   // one K step on stage slot J: this wave's loads of stage kt have landed (the
   // ST-2 newer stages may still be in flight) and its LDS reads are done;
@@ -321,13 +336,13 @@ __global__ __launch_bounds__(256) void gemm_splitk_reduce_kernel(GemmArgs a, int
   epi4<EPI>(a, m, n, sum[0], sum[1], sum[2], sum[3]);
 }
 
-template <int BM, int BN, int WGM, int WGN, int ST, int ROLE>
+template <int BM, int BN, int WGM, int WGN, int ST, int BK, int ROLE>
 hipError_t launch_tile(const GemmArgs& a, int splits, hipStream_t s) {
   const int blocks = ((a.M + BM - 1) / BM) * (a.N / BN);
   constexpr int NT = WGM * WGN * 64;
   if (splits > 1) {
     dim3 grid(blocks, 1, splits);
-    launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, EPI_BIAS, ROLE, true>, grid, NT, 0, s, a);
+    launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, BK, EPI_BIAS, ROLE, true>, grid, NT, 0, s, a);
     const int64_t n4 = (int64_t)a.M * a.N / 4;
     const unsigned rb = (unsigned)((n4 + 255) / 256);
     switch (a.epi) {
@@ -340,17 +355,17 @@ hipError_t launch_tile(const GemmArgs& a, int splits, hipStream_t s) {
   }
   switch (a.epi) {
     case EPI_BIAS:
-      launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, EPI_BIAS, ROLE, false>, blocks, NT, 0, s, a);
+      launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, BK, EPI_BIAS, ROLE, false>, blocks, NT, 0, s, a);
       break;
     case EPI_BIAS_GELU:
-      launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, EPI_BIAS_GELU, ROLE, false>, blocks, NT, 0, s, a);
+      launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, BK, EPI_BIAS_GELU, ROLE, false>, blocks, NT, 0, s, a);
       break;
     case EPI_GATED_RES:
-      launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, EPI_GATED_RES, ROLE, false>, blocks, NT, 0, s, a);
+      launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, BK, EPI_GATED_RES, ROLE, false>, blocks, NT, 0, s, a);
       break;
     case EPI_QKV:
       if constexpr ((BN / WGN) % 64 == 0) {
-        launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, EPI_QKV, ROLE, false>, blocks, NT, 0, s, a);
+        launch_k(gemm_bf16_kernel<BM, BN, WGM, WGN, ST, BK, EPI_QKV, ROLE, false>, blocks, NT, 0, s, a);
       } else {
         return hipErrorInvalidValue;
       }

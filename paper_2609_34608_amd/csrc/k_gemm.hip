@@ -11,32 +11,41 @@ using gemm::launch_tile;
 
 // ---------------------------------------------------------------- configs
 struct TileCfg {
-  int bm, bn, wgm, wgn, st;
+  int bm, bn, wgm, wgn, st, bk;
 };
-// index: tile rows x cols, waves (rows x cols), LDS stages of 32 K
+// index: tile rows x cols, waves (rows x cols), LDS stages, K per stage
 constexpr TileCfg kCfgs[] = {
-    {64, 64, 2, 2, 4},    // 0
-    {64, 128, 2, 2, 4},   // 1
-    {128, 64, 2, 2, 4},   // 2
-    {128, 128, 2, 2, 4},  // 3
-    {256, 256, 2, 4, 4},  // 4
-    {256, 256, 4, 2, 4},  // 5
-    {256, 128, 2, 4, 4},  // 6
-    {128, 256, 2, 4, 4},  // 7
-    {128, 128, 2, 4, 4},  // 8
-    {64, 256, 1, 4, 4},   // 9
-    {64, 64, 2, 2, 8},    // 10
-    {64, 128, 2, 2, 8},   // 11
-    {128, 64, 2, 2, 8},   // 12
-    {64, 64, 2, 2, 12},   // 13
-    {128, 128, 2, 2, 8},  // 14
+    {64, 64, 2, 2, 4, 32},    // 0
+    {64, 128, 2, 2, 4, 32},   // 1
+    {128, 64, 2, 2, 4, 32},   // 2
+    {128, 128, 2, 2, 4, 32},  // 3
+    {256, 256, 2, 4, 4, 32},  // 4
+    {256, 256, 4, 2, 4, 32},  // 5
+    {256, 128, 2, 4, 4, 32},  // 6
+    {128, 256, 2, 4, 4, 32},  // 7
+    {128, 128, 2, 4, 4, 32},  // 8
+    {64, 256, 1, 4, 4, 32},   // 9
+    {64, 64, 2, 2, 8, 32},    // 10
+    {64, 128, 2, 2, 8, 32},   // 11
+    {128, 64, 2, 2, 8, 32},   // 12
+    {64, 64, 2, 2, 12, 32},   // 13
+    {128, 128, 2, 2, 8, 32},  // 14
+    {64, 64, 2, 2, 4, 128},   // 15
+    {64, 128, 2, 2, 3, 128},  // 16
+    {128, 64, 2, 2, 3, 128},  // 17
+    {64, 64, 2, 2, 4, 64},    // 18
+    {64, 128, 2, 2, 4, 64},   // 19
+    {128, 128, 2, 4, 4, 64},  // 20
+    {256, 256, 4, 2, 2, 64},  // 21
+    {256, 256, 2, 4, 2, 64},  // 22
+    {128, 128, 2, 2, 4, 64},  // 23
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
 template <int C, int ROLE>
 hipError_t launch_c(const GemmArgs& a, int splits, hipStream_t s) {
   constexpr TileCfg t = kCfgs[C];
-  return launch_tile<t.bm, t.bn, t.wgm, t.wgn, t.st, ROLE>(a, splits, s);
+  return launch_tile<t.bm, t.bn, t.wgm, t.wgn, t.st, t.bk, ROLE>(a, splits, s);
 }
 
 template <int ROLE>
@@ -56,7 +65,16 @@ hipError_t launch_role(const GemmArgs& a, int cfg, int splits, hipStream_t s) {
     case 11: return launch_c<11, ROLE>(a, splits, s);
     case 12: return launch_c<12, ROLE>(a, splits, s);
     case 13: return launch_c<13, ROLE>(a, splits, s);
-    default: return launch_c<14, ROLE>(a, splits, s);
+    case 14: return launch_c<14, ROLE>(a, splits, s);
+    case 15: return launch_c<15, ROLE>(a, splits, s);
+    case 16: return launch_c<16, ROLE>(a, splits, s);
+    case 17: return launch_c<17, ROLE>(a, splits, s);
+    case 18: return launch_c<18, ROLE>(a, splits, s);
+    case 19: return launch_c<19, ROLE>(a, splits, s);
+    case 20: return launch_c<20, ROLE>(a, splits, s);
+    case 21: return launch_c<21, ROLE>(a, splits, s);
+    case 22: return launch_c<22, ROLE>(a, splits, s);
+    default: return launch_c<23, ROLE>(a, splits, s);
   }
 }
 
@@ -131,17 +149,19 @@ int gemm_num_configs() { return kNumCfgs; }
 
 GemmPlan plan_gemm(int M, int N, int K, int epi) {
   // From a sweep of every configuration at the workload shapes.  Large M:
-  // 256x256 tiles, 8 waves of 64x128 for wide outputs, of 128x64 otherwise.
-  // Small M: 64x64 tiles (64x128 for the QKV epilogue, which needs whole
-  // heads per wave; 128x128 over 8 waves for wide, short-K outputs); a K split
-  // only for grids under half a block per CU.
+  // 256x256 tiles over 8 waves, K 64 per stage (two stages) for outputs wider
+  // than 1024, K 32 per stage (four stages) otherwise.  Small M (under a few
+  // blocks per CU): 64x64 tiles with K 64 per stage, 64x128 for the QKV
+  // epilogue (whole heads per wave), 128x128 over 8 waves for wide, short-K
+  // outputs; a K split only for grids under half a block per CU.
   GemmPlan p{0, 1};
   if (M >= 2048 && N % 256 == 0) {
-    p.cfg = N >= 3072 ? 5 : 4;
+    if (N > 1024 && K % 64 == 0) p.cfg = 22;
+    else p.cfg = N >= 3072 ? 5 : 4;
     return p;
   }
   if (epi == EPI_QKV) {
-    p.cfg = N % 128 == 0 ? 1 : 3;
+    p.cfg = N % 128 != 0 ? 3 : K % 64 == 0 ? 19 : 1;
     return p;
   }
   if (N >= 2048 && N % 128 == 0 && K <= 1024) {
@@ -149,6 +169,10 @@ GemmPlan plan_gemm(int M, int N, int K, int epi) {
     return p;
   }
   const long blocks = (long)((M + 63) / 64) * (N / 64);
+  if (K % 64 == 0 && blocks >= 128) {
+    p.cfg = 18;
+    return p;
+  }
   while (blocks * p.splits < 128 && K / (p.splits * 2) >= 768 && K % (gemm::kBK * p.splits * 2) == 0 &&
          p.splits < 8)
     p.splits *= 2;
@@ -163,7 +187,7 @@ size_t gemm_partial_floats(int M, int N, int K, int epi) {
 hipError_t launch_gemm_cfg(const GemmArgs& a, int cfg, int splits, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   if (cfg < 0 || cfg >= kNumCfgs || splits < 1) return hipErrorInvalidValue;
-  if (a.K % (gemm::kBK * splits) || a.N % kCfgs[cfg].bn || a.N % 4) return hipErrorInvalidValue;
+  if (a.K % (kCfgs[cfg].bk * splits) || a.N % kCfgs[cfg].bn || a.N % 4) return hipErrorInvalidValue;
   if (splits > 1 && (a.epi == EPI_QKV || !a.partial)) return hipErrorInvalidValue;
   if (a.epi == EPI_QKV && !qkv_ok(cfg)) return hipErrorInvalidValue;
   switch (a.role) {
