@@ -242,7 +242,8 @@ typedef struct {
  *   f_mod_w[D][2D] f_mod_b[2D] out_wv[D][Cv] out_bv[Cv] out_wa[D][A] out_ba[A]
  * Returns 0 for an invalid configuration. */
 size_t wam_host_weight_count(const wam_config *cfg);
-/* Device bytes of the packed weights and of the workspace (0 if invalid). */
+/* Device bytes of the packed weights (with the constant position-embedding
+ * table) and of the workspace (0 if invalid). */
 size_t wam_weight_bytes(const wam_config *cfg);
 size_t wam_workspace_bytes(const wam_config *cfg);
 /* Trajectory elements per sample, Nv*Cv + Na*A. */

@@ -101,7 +101,8 @@ __global__ void gemv_reduce_kernel(const float* __restrict__ partial, const floa
 }
 
 // ------------------------------------------------------------- embedding
-// h[b,t,:] = token (video | action | obs) @ W_branch + b_branch + PE(t)
+// h[b,t,:] = token (video | action | obs) @ W_branch + b_branch + PE(t), PE a
+// table built once at init
 __global__ void embed_kernel(EmbedArgs a) {
   const int row = blockIdx.x;  // b*T + t
   const int b = row / a.T, t = row % a.T;
@@ -129,15 +130,11 @@ __global__ void embed_kernel(EmbedArgs a) {
       tok[threadIdx.x] = a.cond[((size_t)b * a.No + (t - a.Nv - a.Na)) * a.Co + threadIdx.x];
   }
   __syncthreads();
-  const int half = a.D / 2;
+  const float* pe = a.pe + (size_t)t * a.D;
   for (int d = threadIdx.x; d < a.D; d += blockDim.x) {
     float s = bias[d];
     for (int j = 0; j < c; ++j) s += tok[j] * w[(size_t)j * a.D + d];
-    const int jj = d < half ? d : d - half;
-    const double om = exp(-log(10000.0) * (double)jj / (double)half);
-    const double ang = (double)t * om;
-    s += (float)(d < half ? sin(ang) : cos(ang));
-    a.h[(size_t)row * a.D + d] = s;
+    a.h[(size_t)row * a.D + d] = s + pe[d];
   }
 }
 

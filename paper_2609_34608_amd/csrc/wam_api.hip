@@ -123,6 +123,7 @@ struct DevLayout {
   size_t bmod;                        // [Nmod] all layers' mod_b then f_mod_b
   size_t lbias0, lbias_stride;        // per layer: qkv_b, proj_b, fc1_b, fc2_b, q_g, k_g
   size_t out_wvT, out_bv, out_waT, out_ba;
+  size_t pe;                          // [T][D] sinusoidal position embedding (a constant table)
   // activation-typed region
   size_t wmod;                        // [D][Nmod]
   size_t lw0, lw_stride;              // per layer: qkv_wT [3D][D], proj_wT [D][D], fc1_wT [F][D], fc2_wT [D][F]
@@ -148,6 +149,7 @@ DevLayout dev_layout(const Dims& d) {
   o += w.lbias_stride * d.L;
   w.out_wvT = f32(D * d.Cv); w.out_bv = f32(d.Cv);
   w.out_waT = f32(D * d.A); w.out_ba = f32(d.A);
+  w.pe = f32((size_t)d.T * D);
   w.wmod = o;
   o = align_up(o + D * d.Nmod * d.act);
   w.lw_stride = align_up((3 * D * D + D * D + F * D + D * F) * d.act);
@@ -337,6 +339,7 @@ int embed(wam_t h, const float* x, const float* cond) {
   a.wv = h->W(wl.in_wv); a.bv = h->W(wl.in_bv);
   a.wa = h->W(wl.in_wa); a.ba = h->W(wl.in_ba);
   a.wo = h->W(wl.in_wo); a.bo = h->W(wl.in_bo);
+  a.pe = h->W(wl.pe);
   a.h = h->S(h->ws.h);
   a.B = d.B; a.T = d.T; a.D = d.D; a.Nv = d.Nv; a.Cv = d.Cv; a.Na = d.Na; a.A = d.A; a.No = d.No; a.Co = d.Co;
   HIPCHK(h, launch_embed(a, h->stream));
@@ -851,6 +854,20 @@ int wam_init(const wam_config* cfg, const float* hw, size_t n_hw, void* dev_weig
   }
   f32(wl.out_bv, hl.out_bv, d.Cv);
   f32(wl.out_ba, hl.out_ba, d.A);
+  {
+    // PE[t][i] = sin(t w_i) for i < D/2, cos(t w_{i-D/2}) above, w_j = 10000^(-j/(D/2)),
+    // evaluated in double and rounded once
+    float* pe = reinterpret_cast<float*>(buf.data() + wl.pe);
+    const int half = d.D / 2;
+    for (int j = 0; j < half; ++j) {
+      const double om = exp(-log(10000.0) * (double)j / (double)half);
+      for (int t = 0; t < d.T; ++t) {
+        const double ang = (double)t * om;
+        pe[(size_t)t * d.D + j] = (float)sin(ang);
+        pe[(size_t)t * d.D + half + j] = (float)cos(ang);
+      }
+    }
+  }
   hipError_t e = hipMemcpy(h->wdev, buf.data(), wl.total, hipMemcpyHostToDevice);
   // pads of q/k/v^T beyond T are read by the attention tiles and must be zero
   if (e == hipSuccess) e = hipMemsetAsync(h->wsdev + ws.q, 0, ws.attn - ws.q, h->stream);

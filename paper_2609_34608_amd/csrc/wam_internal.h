@@ -92,13 +92,16 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-// GELU, tanh form: x/2 (1 + tanh(sqrt(2/pi)(x + 0.044715 x^3))), with
-// tanh(u) = 1 - 2/(exp(2u)+1) written out so that large |u| saturates.
+// GELU, tanh form: x/2 (1 + tanh(u)), u = sqrt(2/pi)(x + 0.044715 x^3),
+// evaluated as x * sigmoid(2u) = x / (1 + 2^(-2u log2 e)) (the same function)
+// with the hardware exp2 and reciprocal (v_exp_f32, v_rcp_f32: about 1 ulp)
+// instead of a correctly rounded division.  Large |u| saturates: 2^(+inf)
+// gives 1/inf = 0, 2^(-inf) gives 1.
 __device__ __forceinline__ float gelu_tanh_f(float x) {
-  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  float u = k0 * (x + 0.044715f * x * x * x);
-  float t = 1.0f - 2.0f / (__expf(2.0f * u) + 1.0f);
-  return 0.5f * x * (1.0f + t);
+  const float c1 = -2.0f * 0.7978845608028654f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
+  const float c3 = c1 * 0.044715f;
+  const float z = x * (c1 + c3 * x * x);
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(z));
 }
 
 // ---------------------------------------------------------------- GEMM
@@ -200,6 +203,7 @@ struct EmbedArgs {
   const float* wv; const float* bv;  // [Cv][D], [D]
   const float* wa; const float* ba;  // [A][D], [D]
   const float* wo; const float* bo;  // [Co][D], [D]
+  const float* pe;    // [T][D] position embedding
   float* h;           // [B][T][D]
   int B, T, D, Nv, Cv, Na, A, No, Co;
 };
