@@ -405,10 +405,11 @@ __global__ __launch_bounds__(kFinalWaves * 64) void final_rows_kernel(FinalArgs 
 }
 
 // ------------------------------------------------------------- Residual Rescaling
-// Per row: sums of p_i p_a, p_i^2, p_a^2 with p_i = h_s - h_q (float64).
+// Per row: sums of p_i p_a, p_i^2, p_a^2 with p_i = h_s - h_q (float64), one
+// wave per row (any D multiple of 4); rr_finish_kernel reduces them.
 __global__ void rr_row_sums_kernel(const float* __restrict__ hs, const float* __restrict__ hq,
-                                   const float* __restrict__ pa, double* __restrict__ out,
-                                   int rows, int D) {
+                                       const float* __restrict__ pa, double* __restrict__ out,
+                                       int rows, int D) {
   const int row = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   if (row >= rows) return;
@@ -435,6 +436,118 @@ __global__ void rr_row_sums_kernel(const float* __restrict__ hs, const float* __
     out[(size_t)row * 3 + 1] = sii;
     out[(size_t)row * 3 + 2] = saa;
   }
+}
+
+// alpha (Eq. crr-alpha), cos and relative fit error (Eq. crr-gate) of one
+// (sample, branch) from its float64 sums over nrows rows of D elements.
+__device__ void rr_gate_stats(const RRGateArgs& a, int b, int br, int nrows, double sip, double sii, double saa) {
+  const double n = (double)nrows * (double)a.D;
+  const double den = fmax(saa / n, (double)a.eps);
+  double alpha = (sip / n) / den;
+  alpha = fmin(fmax(alpha, (double)a.alpha_min), (double)a.alpha_max);
+  const bool ok_norm = sii > 0.0 && saa > 0.0;
+  const double cosv = ok_norm ? sip / sqrt(sii * saa) : 0.0;
+  const double r2 = fmax(sii - 2.0 * alpha * sip + alpha * alpha * saa, 0.0);
+  const double fit = sii > 0.0 ? sqrt(r2) / sqrt(sii) : INFINITY;
+  const bool pass = ok_norm && cosv >= (double)a.gamma_cos && fit <= (double)a.gamma_fit;
+  double* r = a.result + ((size_t)b * 2 + br) * 8;
+  r[0] = sip;
+  r[1] = sii;
+  r[2] = saa;
+  r[3] = alpha;
+  r[4] = cosv;
+  r[5] = fit;
+  r[6] = pass ? 1.0 : 0.0;
+  r[7] = 0.0;
+}
+
+// The gate in two launches, both in fixed summation orders.  Partials: blocks
+// are laid out per (sample, branch): sample b owns gV = ceil(nV / 4) blocks
+// over the rows of branch 0 (rows [0, Nv) then [Nv+Na, T), nV = T - Na of
+// them) followed by gA = ceil(Na / 4) over branch 1 (rows [Nv, Nv+Na)).  Wave
+// w of a block takes one row (all of its loads issued before any
+// arithmetic), and the block adds its rows in wave order into one partial
+// (row_sums[block][3]).  The second kernel, one block per (sample, branch),
+// adds that pair's partials in block order and writes the statistics.
+template <int MAXV>
+__global__ __launch_bounds__(256) void rr_gate_partials_kernel(RRGateArgs a) {
+  const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+  const int nV = a.T - a.Na;
+  const int gV = (nV + 3) / 4, gA = (a.Na + 3) / 4, per = gV + gA;
+  const int b = blockIdx.x / per, j = blockIdx.x % per;
+  const bool br1 = j >= gV;
+  const int i = (br1 ? j - gV : j) * 4 + w;  // row within the branch
+  const bool valid = i < (br1 ? a.Na : nV);
+  const int t = br1 ? a.Nv + i : (i < a.Nv ? i : i + a.Na);
+  __shared__ double part[4][3];
+  double sip = 0.0, sii = 0.0, saa = 0.0;
+  if (valid) {
+    const size_t off = ((size_t)b * a.T + t) * a.D;
+    const int nv = a.D / (4 * kWave);
+    const f32x4* s4 = reinterpret_cast<const f32x4*>(a.hs + off);
+    const f32x4* q4 = reinterpret_cast<const f32x4*>(a.hq + off);
+    const f32x4* a4 = reinterpret_cast<const f32x4*>(a.pa + off);
+    f32x4 sv[MAXV], qv[MAXV], av[MAXV];
+#pragma unroll
+    for (int k = 0; k < MAXV; ++k)
+      if (k < nv) {
+        sv[k] = s4[lane + kWave * k];
+        qv[k] = q4[lane + kWave * k];
+        av[k] = a4[lane + kWave * k];
+      }
+#pragma unroll
+    for (int k = 0; k < MAXV; ++k)
+      if (k < nv) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const double pi = (double)(sv[k][e] - qv[k][e]), pv = (double)av[k][e];
+          sip += pi * pv;
+          sii += pi * pi;
+          saa += pv * pv;
+        }
+      }
+    sip = wave_sum_d(sip);
+    sii = wave_sum_d(sii);
+    saa = wave_sum_d(saa);
+  }
+  if (lane == 0) {
+    part[w][0] = sip;
+    part[w][1] = sii;
+    part[w][2] = saa;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double* out = a.row_sums + (size_t)blockIdx.x * 3;
+    out[0] = (part[0][0] + part[1][0]) + (part[2][0] + part[3][0]);
+    out[1] = (part[0][1] + part[1][1]) + (part[2][1] + part[3][1]);
+    out[2] = (part[0][2] + part[1][2]) + (part[2][2] + part[3][2]);
+  }
+}
+
+__global__ __launch_bounds__(256) void rr_gate_finish_kernel(RRGateArgs a) {
+  const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+  const int b = blockIdx.x / 2, br = blockIdx.x % 2;
+  const int nV = a.T - a.Na;
+  const int gV = (nV + 3) / 4, gA = (a.Na + 3) / 4, per = gV + gA;
+  const int first = b * per + (br ? gV : 0), cnt = br ? gA : gV;
+  double s[3] = {0.0, 0.0, 0.0};
+#pragma unroll 8
+  for (int k = threadIdx.x; k < cnt; k += 256) {
+    const double* p = a.row_sums + (size_t)(first + k) * 3;
+    s[0] += p[0];
+    s[1] += p[1];
+    s[2] += p[2];
+  }
+  __shared__ double sh[3][4];
+#pragma unroll
+  for (int c = 0; c < 3; ++c) {
+    const double v = wave_sum_d(s[c]);
+    if (lane == 0) sh[c][w] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0)
+    rr_gate_stats(a, b, br, br ? a.Na : nV, (sh[0][0] + sh[0][1]) + (sh[0][2] + sh[0][3]),
+                  (sh[1][0] + sh[1][1]) + (sh[1][2] + sh[1][3]), (sh[2][0] + sh[2][1]) + (sh[2][2] + sh[2][3]));
 }
 
 // One block per (sample, branch): alpha (Eq. crr-alpha), cos and relative
@@ -467,45 +580,47 @@ __global__ __launch_bounds__(1024) void rr_finish_kernel(RRGateArgs a) {
     sii += sh[1][i];
     saa += sh[2][i];
   }
-  const double n = (double)nrows * (double)a.D;
-  const double den = fmax(saa / n, (double)a.eps);
-  double alpha = (sip / n) / den;
-  alpha = fmin(fmax(alpha, (double)a.alpha_min), (double)a.alpha_max);
-  const bool ok_norm = sii > 0.0 && saa > 0.0;
-  const double cosv = ok_norm ? sip / sqrt(sii * saa) : 0.0;
-  const double r2 = fmax(sii - 2.0 * alpha * sip + alpha * alpha * saa, 0.0);
-  const double fit = sii > 0.0 ? sqrt(r2) / sqrt(sii) : INFINITY;
-  const bool pass = ok_norm && cosv >= (double)a.gamma_cos && fit <= (double)a.gamma_fit;
-  double* r = a.result + ((size_t)b * 2 + br) * 8;
-  r[0] = sip;
-  r[1] = sii;
-  r[2] = saa;
-  r[3] = alpha;
-  r[4] = cosv;
-  r[5] = fit;
-  r[6] = pass ? 1.0 : 0.0;
-  r[7] = 0.0;
+  rr_gate_stats(a, b, br, nrows, sip, sii, saa);
 }
 
 // h_e = h_s + alpha_{b,branch} R_a (Eq. residual-injection), in place on h.
-__global__ void rr_inject_kernel(float* __restrict__ h, const float* __restrict__ Ra,
-                                 const double* __restrict__ result, int rows, int T, int D,
-                                 int Nv, int Na, const int* flag) {
+// A thread updates kInjV float4 spaced one block width apart (all loads
+// first; in the model one per thread measured fastest).  A float4 never
+// straddles rows (D % 4 == 0); its sample and branch come from comparisons
+// against the float4 offsets of the sample and branch boundaries (host:
+// rows * D / 4 < 2^31).
+constexpr int kInjV = 1;
+__global__ __launch_bounds__(256) void rr_inject_kernel(float* __restrict__ h, const float* __restrict__ Ra,
+                                                        const double* __restrict__ result, int B, int T, int D,
+                                                        int Nv, int Na, const int* flag) {
   if (flag && *flag != 1) return;
-  const int64_t i4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t n4 = (int64_t)rows * D / 4;
-  if (i4 >= n4) return;
-  const int row = (int)((i4 * 4) / D);
-  const int b = row / T, t = row % T;
-  const int br = (t >= Nv && t < Nv + Na) ? 1 : 0;
-  const float al = (float)result[((size_t)b * 2 + br) * 8 + 3];
-  float4 hv = reinterpret_cast<float4*>(h)[i4];
-  const float4 rv = reinterpret_cast<const float4*>(Ra)[i4];
-  hv.x += al * rv.x;
-  hv.y += al * rv.y;
-  hv.z += al * rv.z;
-  hv.w += al * rv.w;
-  reinterpret_cast<float4*>(h)[i4] = hv;
+  const int d4 = D / 4, td4 = T * d4, n4 = B * td4, lo = Nv * d4, hi = (Nv + Na) * d4;
+  const int base = blockIdx.x * (256 * kInjV) + threadIdx.x;
+  f32x4* h4 = reinterpret_cast<f32x4*>(h);
+  const f32x4* r4 = reinterpret_cast<const f32x4*>(Ra);
+  f32x4 hv[kInjV], rv[kInjV];
+#pragma unroll
+  for (int u = 0; u < kInjV; ++u) {
+    const int i4 = base + 256 * u;
+    if (i4 < n4) {
+      hv[u] = h4[i4];
+      rv[u] = r4[i4];
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kInjV; ++u) {
+    const int i4 = base + 256 * u;
+    if (i4 < n4) {
+      int b = 0, r = i4;
+      while (r >= td4) {
+        r -= td4;
+        ++b;
+      }
+      const int br = (r >= lo && r < hi) ? 1 : 0;
+      const float al = (float)result[((size_t)b * 2 + br) * 8 + 3];
+      h4[i4] = hv[u] + al * rv[u];
+    }
+  }
 }
 
 __global__ void rr_pre_middle_kernel(const float* __restrict__ h, float* __restrict__ hq,
@@ -570,6 +685,19 @@ __global__ void pack_condition_kernel(const float* __restrict__ obs, int n_obs, 
 __global__ void copy_f32_kernel(const float* __restrict__ src, float* __restrict__ dst, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) dst[i] = src[i];
+}
+
+// float4 copy, four per thread spaced one block width apart (n4 float4)
+__global__ __launch_bounds__(256) void copy_f32x4_kernel(const f32x4* __restrict__ src, f32x4* __restrict__ dst,
+                                                         int64_t n4) {
+  const int64_t base = (int64_t)blockIdx.x * 1024 + threadIdx.x;
+  f32x4 v[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+    if (base + 256 * u < n4) v[u] = src[base + 256 * u];
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+    if (base + 256 * u < n4) dst[base + 256 * u] = v[u];
 }
 
 // ------------------------------------------------------------- Trajectory Remapping
@@ -712,6 +840,12 @@ hipError_t launch_rr_gate(const RRGateArgs& a, hipStream_t s) {
   const int rows = a.B * a.T;
   if (a.D % 4) return hipErrorInvalidValue;
   const int wpb = 4;
+  if (a.D % 256 == 0 && a.D <= 2048) {
+    const int per = (a.T - a.Na + 3) / 4 + (a.Na + 3) / 4;
+    launch_k(rr_gate_partials_kernel<8>, (unsigned)(a.B * per), 256, 0, s, a);
+    launch_k(rr_gate_finish_kernel, (unsigned)(a.B * 2), 256, 0, s, a);
+    return hipGetLastError();
+  }
   launch_k(rr_row_sums_kernel, (rows + wpb - 1) / wpb, wpb * kWave, 0, s, a.hs, a.hq, a.pa, a.row_sums, rows, a.D);
   launch_k(rr_finish_kernel, a.B * 2, 1024, 0, s, a);
   return hipGetLastError();
@@ -720,7 +854,9 @@ hipError_t launch_rr_gate(const RRGateArgs& a, hipStream_t s) {
 hipError_t launch_rr_inject(float* h, const float* Ra, const double* result, int B, int T, int D,
                             int Nv, int Na, hipStream_t s, const int* flag) {
   const int64_t n4 = (int64_t)B * T * D / 4;
-  launch_k(rr_inject_kernel, (unsigned)((n4 + 255) / 256), 256, 0, s, h, Ra, result, B * T, T, D, Nv, Na, flag);
+  if (D % 4 || n4 >= (int64_t)1 << 31) return hipErrorInvalidValue;
+  const unsigned grid = (unsigned)((n4 + 256 * kInjV - 1) / (256 * kInjV));
+  launch_k(rr_inject_kernel, grid, 256, 0, s, h, Ra, result, B, T, D, Nv, Na, flag);
   return hipGetLastError();
 }
 
@@ -755,7 +891,13 @@ hipError_t launch_pack_condition(const float* obs, int n_obs, int c_obs, const f
 
 hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  launch_k(copy_f32_kernel, (unsigned)((n + 255) / 256), 256, 0, s, src, dst, n);
+  if (n % 4 == 0 && reinterpret_cast<uintptr_t>(src) % 16 == 0 && reinterpret_cast<uintptr_t>(dst) % 16 == 0) {
+    const int64_t n4 = n / 4;
+    launch_k(copy_f32x4_kernel, (unsigned)((n4 + 1023) / 1024), 256, 0, s, reinterpret_cast<const f32x4*>(src),
+             reinterpret_cast<f32x4*>(dst), n4);
+  } else {
+    launch_k(copy_f32_kernel, (unsigned)((n + 255) / 256), 256, 0, s, src, dst, n);
+  }
   return hipGetLastError();
 }
 

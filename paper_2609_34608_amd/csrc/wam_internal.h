@@ -234,7 +234,7 @@ struct RRGateArgs {
   const float* hs;   // h_s [M][D]
   const float* hq;   // h_q
   const float* pa;   // retained p_a
-  double* row_sums;  // [M][3]: sum p_i p_a, sum p_i^2, sum p_a^2
+  double* row_sums;  // [M][3]: per-row (or per-block) sums p_i p_a, p_i^2, p_a^2
   double* result;    // [B][2][8]: Sip Sii Saa alpha cos fit pass pad
   int B, T, D, Nv, Na;
   float alpha_min, alpha_max, eps, gamma_cos, gamma_fit;

@@ -111,6 +111,12 @@ TINY_RR = _reg(TINY.replace(
     name="tiny_rr", L=4, rr_bounds=(1, 2, 3),
     notes="tiny fp32 DiT with 4 layers for residual-rescaling tests"))
 
+# The same with hidden 256 (head size 64): rows of a width that the
+# residual-rescaling gate's per-block partial kernels take (multiples of 256).
+TINY_RR256 = _reg(TINY_RR.replace(
+    name="tiny_rr256", D=256, H=4,
+    notes="tiny fp32 DiT, 4 layers, hidden 256, for the partial-sum residual-rescaling gate"))
+
 # Small bf16 model: 12 layers, hidden 768, 12 heads, MLP 3072; 3 frames of
 # 16x16 patches = 768 video tokens + 32 action tokens (7-dim) + 64 obs tokens;
 # 10 flow steps; reuse continues from step 5.

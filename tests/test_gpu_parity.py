@@ -103,10 +103,16 @@ def test_determinism(dev):
 
 
 # ------------------------------------------------------------------ Residual Rescaling
+# hidden 128 takes the per-row gate kernels, hidden 256 (a multiple of 256)
+# the per-block partial gate kernels
+_RR_MODELS = ["tiny_rr", "tiny_rr256"]
+
+
+@pytest.mark.parametrize("model", _RR_MODELS)
 @pytest.mark.parametrize("mode_name", ["AUTO", "FORCE_SKIP", "FORCE_FULL", "NEVER"])
-def test_rr_modes_match_oracle(dev, mode_name):
+def test_rr_modes_match_oracle(dev, mode_name, model):
     from paper_2609_34608_amd import _lib as L
-    spec, W, m, sig = _tiny(dev, "tiny_rr", B=2)
+    spec, W, m, sig = _tiny(dev, model, B=2)
     modes = {"AUTO": (L.WAM_RR_AUTO, {}), "FORCE_SKIP": (L.WAM_RR_FORCE_SKIP, {}),
              "FORCE_FULL": (L.WAM_RR_FORCE_FULL, {}), "NEVER": (L.WAM_RR_AUTO, {"gamma_cos": 1.5})}
     mode, kw = modes[mode_name]
@@ -133,10 +139,11 @@ def test_rr_modes_match_oracle(dev, mode_name):
         assert all(i.accepted for i in infos[1:])
 
 
-def test_rr_identity_adaptation(dev):
+@pytest.mark.parametrize("model", _RR_MODELS)
+def test_rr_identity_adaptation(dev, model):
     """The same step twice: the second reuses with alpha = 1, cos = 1, fit ~ 0."""
     from paper_2609_34608_amd import _lib as L
-    spec, W, m, sig = _tiny(dev, "tiny_rr", B=2)
+    spec, W, m, sig = _tiny(dev, model, B=2)
     rr_g, _ = rr_of(spec, L.WAM_RR_AUTO)
     x0 = to_dev(make_initial_noise(spec), dev)
     c = to_dev(make_observations(spec, 0)[0], dev)
@@ -151,12 +158,13 @@ def test_rr_identity_adaptation(dev):
     assert rel_err(v2.cpu().numpy(), v1.cpu().numpy()) <= 1e-5
 
 
+@pytest.mark.parametrize("model", _RR_MODELS)
 @pytest.mark.parametrize("mode_name", ["AUTO", "FORCE_SKIP", "FORCE_FULL", "NEVER", "MIXED"])
-def test_device_decision_matches_host_decision(dev, mode_name):
+def test_device_decision_matches_host_decision(dev, mode_name, model):
     """The device-resident decision runs the same kernels in the same order:
     bit-identical trajectories and identical step reports."""
     from paper_2609_34608_amd import _lib as L
-    spec, W, m, sig = _tiny(dev, "tiny_rr", B=2)
+    spec, W, m, sig = _tiny(dev, model, B=2)
     modes = {"AUTO": (L.WAM_RR_AUTO, {}), "FORCE_SKIP": (L.WAM_RR_FORCE_SKIP, {}),
              "FORCE_FULL": (L.WAM_RR_FORCE_FULL, {}), "NEVER": (L.WAM_RR_AUTO, {"gamma_cos": 1.5}),
              "MIXED": (L.WAM_RR_AUTO, {"gamma_cos": 0.0, "gamma_fit": 1.02})}
