@@ -270,6 +270,52 @@ def test_closed_loop_replans_match_oracle(dev, tau, graphs):
         assert all(p == L.WAM_PATH_REJECT for p in paths[1:])
 
 
+def test_small_replay_replans_match_oracle(dev):
+    """The closed-loop replay workload itself (small bf16 model, action shift
+    8, AR(1) observations, TR + OR + RR): three replans, teacher-forced per
+    replan as above, each action chunk within 2e-2 of the oracle.  The first
+    replan runs all 10 steps; the next two are accepted rebindings (S < tau),
+    2 prefix steps under the predicted observation and 3 under the real one."""
+    from paper_2609_34608_amd import _lib as L
+    spec, W, m = model_for("replay", dev)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    rr_g, rr_o = rr_of(spec, L.WAM_RR_AUTO)
+    ra = _replan_args(spec)
+    rho = spec.ar_rho
+    delta = 1.0 / np.sqrt(1 - rho * rho)
+    n_ctrl = 3
+    obs = make_observations(spec, n_ctrl)
+    m.reset_all()
+    rt = OM.ReplanRuntime(W, spec, sig, rr_o, OM.RuntimeProfile(**ra))
+    x_out = m.new_traj()
+    paths = []
+    for t in range(n_ctrl):
+        c_real = obs[t]
+        c_pred = (rho * obs[t - 1]).astype(np.float32) if t > 0 else obs[t]
+        if t > 0:
+            xb, xr, kappa = m.get_replan_state()
+            rt.set_state(xb.cpu().numpy(), xr.cpu().numpy(), kappa)
+        cr, cp = to_dev(c_real, dev), to_dev(c_pred, dev)
+        info = m.replan(cr, x_out, to_dev(make_remap_noise(spec, t), dev), cond_pred=cp, u_hat=[cp], u=[cr],
+                        delta=[delta], weight=[1.0], noise_first=to_dev(make_initial_noise(spec), dev),
+                        rr=rr_g, **ra)
+        trace = deque(int(d) for d in info.decision[:info.steps] if d >= 0)
+        ref, rinfo = rt.replan(c_real, c_pred, [c_pred], [c_real], [delta], [1.0],
+                               noise_first=make_initial_noise(spec), noise_remap=make_remap_noise(spec, t),
+                               forced=trace)
+        assert info.path == rinfo.path, t
+        assert info.steps == rinfo.steps and info.kappa == rinfo.kappa
+        if rinfo.S is not None:
+            assert info.S == pytest.approx(rinfo.S, rel=1e-6)
+        got = x_out.cpu().numpy()
+        e = rel_err(OM.action_chunk(spec, got), OM.action_chunk(spec, ref))
+        print(f"replay replan {t}: path {info.path}, {info.steps} steps, action chunk rel err {e:.3e}")
+        assert e <= BF16_TOL, (t, e)
+        paths.append(info.path)
+    assert paths == [L.WAM_PATH_FIRST, L.WAM_PATH_ACCEPT, L.WAM_PATH_ACCEPT]
+
+
 # ------------------------------------------------------------------ bf16 workloads
 def test_small_bf16_native_chunk(dev):
     spec, W, m = model_for("small", dev)
