@@ -56,7 +56,8 @@ def kernel_class(name: str):
     if m:
         return CLASS_NAMES[int(m.group(1))]
     for key, cls in (("attn_bf16", "attention"), ("rr_row_sums_kernel", "rr_gate"),
-                     ("rr_finish_kernel", "rr_gate"), ("rr_inject_kernel", "rr_inject"),
+                     ("rr_finish_kernel", "rr_gate"), ("rr_gate_partials_kernel", "rr_gate"),
+                     ("rr_gate_finish_kernel", "rr_gate"), ("rr_inject_kernel", "rr_inject"),
                      ("rr_refresh_kernel", "rr_refresh")):
         if key in name:
             return cls

@@ -86,6 +86,19 @@ constexpr int kPingPong = 88;
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void global_void;
 
+// Query block and (sample, head) of this workgroup.  Workgroups go to the 8
+// XCDs round-robin by linear id; renumbering them so that each XCD takes a
+// contiguous run of (head, query block) pairs keeps all query blocks of a
+// head on one XCD, whose L2 then fetches that head's K and V^T once.
+__device__ __forceinline__ void attn_block(int& qb, int& bh) {
+  const int nqb = gridDim.x, nb = gridDim.x * gridDim.y;
+  const int lin = blockIdx.y * nqb + blockIdx.x;
+  const int per = nb / 8, rem = nb % 8, x = lin % 8, idx = lin / 8;
+  const int logical = x * per + min(x, rem) + idx;
+  qb = logical % nqb;
+  bh = logical / nqb;
+}
+
 // s_waitcnt immediate (gfx9 layout): at most n vector-memory operations and no
 // LDS operation outstanding
 constexpr int waitcnt_vm_lgkm0(int n) { return (n & 0xf) | ((n >> 4) << 14) | (0x7 << 4); }
@@ -102,10 +115,11 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   // stage: 128 rows of 64 bf16 (128 bytes); chunk c of row r stored at c ^ (r & 7)
   __shared__ __attribute__((aligned(1024))) bf16 sm[ST][128 * kDh];
 
-  const int bh = blockIdx.y;
+  int qb, bh;
+  attn_block(qb, bh);
   const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, lane = tid % 64, wid = tid / 64;
-  const int q0 = blockIdx.x * QB + wid * QT * 16;
+  const int q0 = qb * QB + wid * QT * 16;
   const int g = lane / 16, lr = lane % 16;
 
   const bf16* Q = static_cast<const bf16*>(a.q) + (size_t)bh * a.Tpad * kDh;
@@ -321,10 +335,11 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_bounded_kernel(AttnArgs a) 
   if (a.skip && *a.skip) return;
   __shared__ __attribute__((aligned(1024))) bf16 sm[ST][128 * kDh];
 
-  const int bh = blockIdx.y;
+  int qb, bh;
+  attn_block(qb, bh);
   const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, lane = tid % 64, wid = tid / 64;
-  const int q0 = blockIdx.x * QB + wid * QT * 16;
+  const int q0 = qb * QB + wid * QT * 16;
   const int g = lane / 16, lr = lane % 16;
 
   const bf16* Q = static_cast<const bf16*>(a.q) + (size_t)bh * a.Tpad * kDh;
@@ -510,11 +525,12 @@ __global__ __launch_bounds__(512) void attn_bf16_pingpong_kernel(AttnArgs a) {
   if (a.skip && *a.skip) return;
   __shared__ __attribute__((aligned(1024))) bf16 sm[ST][128 * kDh];
 
-  const int bh = blockIdx.y;
+  int qb, bh;
+  attn_block(qb, bh);
   const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, lane = tid % 64, wid = tid / 64;
   const bool grp1 = wid >= 4;
-  const int q0 = blockIdx.x * QB + wid * QT * 16;
+  const int q0 = qb * QB + wid * QT * 16;
   const int g = lane / 16, lr = lane % 16;
 
   const bf16* Q = static_cast<const bf16*>(a.q) + (size_t)bh * a.Tpad * kDh;
