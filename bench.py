@@ -28,7 +28,7 @@ sys.path.insert(0, ROOT)
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
 HBM_PEAK_GBS = 8000.0
-ATTN_VARIANTS = {"auto": 0, "running": 1, "bounded": 2, "pingpong": 3}
+ATTN_VARIANTS = {"auto": 0, "running": 1, "bounded": 2, "pingpong": 3, "plain": 4}
 CLASS_NAMES = ["gemm_qkv", "gemm_proj", "gemm_fc1", "gemm_fc2", "attention", "rr_gate", "rr_inject",
                "rr_refresh"]
 
@@ -128,9 +128,10 @@ def parse():
                    help="residual-rescaling mode of the timed replans")
     p.add_argument("--exec", default="host", choices=["host", "device", "graph"],
                    help="RR decision on the host, on the device, or on the device with graph replay")
-    p.add_argument("--attention", default="auto", choices=["auto", "running", "bounded", "pingpong"],
+    p.add_argument("--attention", default="auto", choices=list(ATTN_VARIANTS),
                    help="bf16 attention kernel: auto, running-max softmax, bounded (fixed reference from the "
-                        "QK-norm score bound), or the bounded ping-pong form")
+                        "QK-norm score bound, software-pipelined), the bounded ping-pong form, or the "
+                        "bounded plain loop")
     p.add_argument("--copy-probe-mib", type=int, default=0,
                    help="one plain device copy of this size before timing (PMC calibration)")
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),

@@ -99,14 +99,20 @@ extern "C" {
 #define WAM_OPT_ATTENTION 3       /* bf16 attention kernel (WAM_ATTN_*); every form
                                      gives the same result up to rounding */
 #define WAM_ATTN_AUTO 0           /* default: a bounded form where the layer allows
-                                     it (ping-pong for long sequences), else the
-                                     running max */
+                                     it (tile shape chosen by sequence length and
+                                     grid size), else the running max */
 #define WAM_ATTN_RUNNING_MAX 1    /* online softmax with a running maximum          */
 #define WAM_ATTN_BOUNDED 2        /* QK-norm bounds every score by mref <= 60 (log2
                                      units, from the gains): mref is the fixed
-                                     softmax reference, no running max             */
+                                     softmax reference, no running max; software-
+                                     pipelined loop (QK of the next key tile
+                                     issued before PV of this one)                 */
 #define WAM_ATTN_PINGPONG 3       /* bounded, 8 waves in two groups that alternate
                                      MFMA and exp2 phases on each SIMD            */
+#define WAM_ATTN_PLAIN 4          /* bounded, plain loop (one score buffer, more
+                                     waves per SIMD)                              */
+/* A bounded form asked for on a layer whose gains allow no bound (mref > 60)
+   runs the running-max kernel. */
 
 #define WAM_MAX_BATCH 16
 #define WAM_MAX_COMPONENTS 8

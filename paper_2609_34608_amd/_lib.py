@@ -20,7 +20,7 @@ WAM_ADAPT_REMAP, WAM_ADAPT_RESET_LAYER, WAM_ADAPT_RESET_ALL, WAM_ADAPT_SET_REPLA
 WAM_PATH_FIRST, WAM_PATH_ACCEPT, WAM_PATH_REJECT, WAM_PATH_FORCED, WAM_PATH_DIRECT = 0, 1, 2, 3, 4
 WAM_MAX_BATCH, WAM_MAX_COMPONENTS, WAM_MAX_STEPS = 16, 8, 64
 WAM_OPT_DEVICE_DECISION, WAM_OPT_GRAPHS, WAM_OPT_ATTENTION = 1, 2, 3
-WAM_ATTN_AUTO, WAM_ATTN_RUNNING_MAX, WAM_ATTN_BOUNDED, WAM_ATTN_PINGPONG = 0, 1, 2, 3
+WAM_ATTN_AUTO, WAM_ATTN_RUNNING_MAX, WAM_ATTN_BOUNDED, WAM_ATTN_PINGPONG, WAM_ATTN_PLAIN = 0, 1, 2, 3, 4
 (WAM_KC_GEMM_QKV, WAM_KC_GEMM_PROJ, WAM_KC_GEMM_FC1, WAM_KC_GEMM_FC2, WAM_KC_ATTENTION,
  WAM_KC_RR_GATE, WAM_KC_RR_INJECT, WAM_KC_RR_REFRESH, WAM_KC_COUNT) = range(9)
 

@@ -80,8 +80,6 @@ constexpr int kDh = 64;
 constexpr int kKB = 64;  // keys per tile
 // largest fixed softmax reference: p >= 2^(-2 mref) must stay a normal float
 constexpr float kMaxBoundedRef = 60.0f;
-// launch_attention_cfg's wave-count value that selects the ping-pong kernel
-constexpr int kPingPong = 88;
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void global_void;
@@ -104,7 +102,10 @@ __device__ __forceinline__ void attn_block(int& qb, int& bh) {
 constexpr int waitcnt_vm_lgkm0(int n) { return (n & 0xf) | ((n >> 4) << 14) | (0x7 << 4); }
 __device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
 
-template <int QT, int NW, int ST>
+// BND: the fixed reference of the bounded kernels (a.mref) instead of the
+// running max, in this plain (not software-pipelined) loop, which needs one
+// score buffer and so leaves room for more waves per SIMD.
+template <int QT, int NW, int ST, bool BND = false>
 __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   constexpr int QB = NW * QT * 16;  // queries per block
   constexpr int NI = 16;            // 1 KiB load instructions per stage: K rows 0-63, V^T rows 64-127
@@ -185,7 +186,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
       const bf16x8 k1f = *reinterpret_cast<const bf16x8*>(krow + (((g + 4) ^ sw) * 8));
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt) {
-        const float nm = -mrun[qt];
+        const float nm = BND ? -a.mref : -mrun[qt];
         f32x4 z = {nm, nm, nm, nm};
         z = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k0f, qf[qt][0], z, 0, 0, 0);
         s[kt][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(k1f, qf[qt][1], z, 0, 0, 0);
@@ -203,6 +204,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
           for (int qt = 0; qt < QT; ++qt) s[kt][qt][r] = live ? s[kt][qt][r] : -INFINITY;
         }
     }
+    if constexpr (!BND) {
     // online softmax per query column (lane-local except the max)
     float mx[QT];
     bool grow = false;
@@ -233,6 +235,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt) s[kt][qt] -= delta;
       }
+    }
     }
     // V^T operands: with the stored key order the eight keys of slot (c, g)
     // are chunk 4c + g of the V^T row
@@ -772,41 +775,51 @@ hipError_t launch_qkv_relayout(const RelayoutArgs& a, bool bf16_mode, hipStream_
 // grid for qt query tiles per wave and nw waves per block
 // (qt, nw, st): query tiles of 16 per wave, waves per block, LDS stages of
 // one 64-key K / V^T tile.  Only the instantiated combinations are accepted.
-hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int st, hipStream_t s, bool bounded) {
+hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int st, hipStream_t s, int form) {
   // every key tile but the last is fully inside [0, T), the last holds >= 1 key
   if (a.dh != kDh || a.T <= 0 || a.Tpad % kKB || a.T > a.Tpad || a.T <= a.Tpad - kKB) return hipErrorInvalidValue;
-  const int qb = qt * (nw == kPingPong ? 8 : nw) * 16;
+  if (form != ATTN_RUNNING && (!a.bounded || !(a.mref >= 0.f && a.mref <= kMaxBoundedRef))) return hipErrorInvalidValue;
+  if (form == ATTN_PINGPONG) nw = 8;
+  const int qb = qt * nw * 16;
   const dim3 grid((a.T + qb - 1) / qb, a.B * a.H);
   const int key = qt * 10000 + nw * 100 + st;
-  if (bounded) {
-    if (!a.bounded || !(a.mref >= 0.f && a.mref <= kMaxBoundedRef)) return hipErrorInvalidValue;
-    switch (key) {
-      case 10404: launch_k(attn_bf16_bounded_kernel<1, 4, 4>, grid, 256, 0, s, a); break;
-      case 20404: launch_k(attn_bf16_bounded_kernel<2, 4, 4>, grid, 256, 0, s, a); break;
-      case 20403: launch_k(attn_bf16_bounded_kernel<2, 4, 3>, grid, 256, 0, s, a); break;
-      case 10204: launch_k(attn_bf16_bounded_kernel<1, 2, 4>, grid, 128, 0, s, a); break;
-      case 20804: launch_k(attn_bf16_bounded_kernel<2, 8, 4>, grid, 512, 0, s, a); break;
-      case 40404: launch_k(attn_bf16_bounded_kernel<4, 4, 4>, grid, 256, 0, s, a); break;
-      // ping-pong kernel: nw = kPingPong (8 waves in two groups)
-      case 28804: launch_k(attn_bf16_pingpong_kernel<2, 4>, grid, 512, 0, s, a); break;
-      case 28805: launch_k(attn_bf16_pingpong_kernel<2, 5>, grid, 512, 0, s, a); break;
-      case 18804: launch_k(attn_bf16_pingpong_kernel<1, 4>, grid, 512, 0, s, a); break;
-      case 48804: launch_k(attn_bf16_pingpong_kernel<4, 4>, grid, 512, 0, s, a); break;
-      case 38804: launch_k(attn_bf16_pingpong_kernel<3, 4>, grid, 512, 0, s, a); break;
-      default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
-  }
-  switch (key) {
-    case 10404: launch_k(attn_bf16_kernel<1, 4, 4>, grid, 256, 0, s, a); break;
-    case 20404: launch_k(attn_bf16_kernel<2, 4, 4>, grid, 256, 0, s, a); break;
-    case 40403: launch_k(attn_bf16_kernel<4, 4, 3>, grid, 256, 0, s, a); break;
-    case 10804: launch_k(attn_bf16_kernel<1, 8, 4>, grid, 512, 0, s, a); break;
-    case 20804: launch_k(attn_bf16_kernel<2, 8, 4>, grid, 512, 0, s, a); break;
-    case 20803: launch_k(attn_bf16_kernel<2, 8, 3>, grid, 512, 0, s, a); break;
-    case 40402: launch_k(attn_bf16_kernel<4, 4, 2>, grid, 256, 0, s, a); break;
-    case 20402: launch_k(attn_bf16_kernel<2, 4, 2>, grid, 256, 0, s, a); break;
-    default: return hipErrorInvalidValue;
+  switch (form) {
+    case ATTN_PIPELINED:
+      switch (key) {
+        case 10404: launch_k(attn_bf16_bounded_kernel<1, 4, 4>, grid, 256, 0, s, a); break;
+        case 20404: launch_k(attn_bf16_bounded_kernel<2, 4, 4>, grid, 256, 0, s, a); break;
+        case 20403: launch_k(attn_bf16_bounded_kernel<2, 4, 3>, grid, 256, 0, s, a); break;
+        default: return hipErrorInvalidValue;
+      }
+      break;
+    case ATTN_PLAIN:
+      switch (key) {
+        case 20402: launch_k(attn_bf16_kernel<2, 4, 2, true>, grid, 256, 0, s, a); break;
+        case 20403: launch_k(attn_bf16_kernel<2, 4, 3, true>, grid, 256, 0, s, a); break;
+        case 40802: launch_k(attn_bf16_kernel<4, 8, 2, true>, grid, 512, 0, s, a); break;
+        case 10402: launch_k(attn_bf16_kernel<1, 4, 2, true>, grid, 256, 0, s, a); break;
+        default: return hipErrorInvalidValue;
+      }
+      break;
+    case ATTN_PINGPONG:
+      switch (key) {
+        case 40804: launch_k(attn_bf16_pingpong_kernel<4, 4>, grid, 512, 0, s, a); break;
+        case 20804: launch_k(attn_bf16_pingpong_kernel<2, 4>, grid, 512, 0, s, a); break;
+        default: return hipErrorInvalidValue;
+      }
+      break;
+    default:
+      switch (key) {
+        case 10404: launch_k(attn_bf16_kernel<1, 4, 4>, grid, 256, 0, s, a); break;
+        case 20404: launch_k(attn_bf16_kernel<2, 4, 4>, grid, 256, 0, s, a); break;
+        case 40403: launch_k(attn_bf16_kernel<4, 4, 3>, grid, 256, 0, s, a); break;
+        case 10804: launch_k(attn_bf16_kernel<1, 8, 4>, grid, 512, 0, s, a); break;
+        case 20804: launch_k(attn_bf16_kernel<2, 8, 4>, grid, 512, 0, s, a); break;
+        case 20803: launch_k(attn_bf16_kernel<2, 8, 3>, grid, 512, 0, s, a); break;
+        case 40402: launch_k(attn_bf16_kernel<4, 4, 2>, grid, 256, 0, s, a); break;
+        case 20402: launch_k(attn_bf16_kernel<2, 4, 2>, grid, 256, 0, s, a); break;
+        default: return hipErrorInvalidValue;
+      }
   }
   return hipGetLastError();
 }
@@ -825,21 +838,26 @@ float attention_score_bound(const float* q_g, const float* k_g) {
 
 hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s) {
   if (bf16_mode && a.bounded && a.variant != WAM_ATTN_RUNNING_MAX) {
-    // ping-pong (512 queries per block) for long sequences that still give
-    // about two blocks per CU; otherwise 128 or 64 queries per block
-    const long bpp = (long)((a.T + 511) / 512) * a.B * a.H;
-    if (a.variant == WAM_ATTN_PINGPONG || (a.variant == WAM_ATTN_AUTO && a.T >= 4096 && bpp >= 384))
-      return launch_attention_cfg(a, 4, kPingPong, 4, s, true);
-    const long blocks = (long)((a.T + 127) / 128) * a.B * a.H;
-    if (blocks >= 256) return launch_attention_cfg(a, 2, 4, 4, s, true);
-    return launch_attention_cfg(a, 1, 4, 4, s, true);
+    if (a.variant == WAM_ATTN_PINGPONG) return launch_attention_cfg(a, 4, 8, 4, s, ATTN_PINGPONG);
+    // from a sweep at the workload shapes: long sequences with about two
+    // blocks of 512 queries per CU take 8 waves of 64 queries; 4 waves of 32
+    // queries when that fills the chip; short grids 4 waves of 16 queries,
+    // where the pipelined loop hides the most latency
+    const bool big = a.T >= 4096 && (long)((a.T + 511) / 512) * a.B * a.H >= 384;
+    const bool full = (long)((a.T + 127) / 128) * a.B * a.H >= 256;
+    if (a.variant == WAM_ATTN_BOUNDED)
+      return full ? launch_attention_cfg(a, 2, 4, 4, s, ATTN_PIPELINED) : launch_attention_cfg(a, 1, 4, 4, s, ATTN_PIPELINED);
+    if (big) return launch_attention_cfg(a, 4, 8, 2, s, ATTN_PLAIN);
+    if (full) return launch_attention_cfg(a, 2, 4, 2, s, ATTN_PLAIN);
+    if (a.variant == WAM_ATTN_PLAIN) return launch_attention_cfg(a, 1, 4, 2, s, ATTN_PLAIN);
+    return launch_attention_cfg(a, 1, 4, 4, s, ATTN_PIPELINED);
   }
   if (bf16_mode) {
     // 4 waves x 32 queries (two K/V stages) when that fills the chip, else
     // 4 waves x 16 queries
     const long blocks = (long)((a.T + 255) / 256) * a.B * a.H;
-    if (blocks >= 256) return launch_attention_cfg(a, 2, 4, 2, s);
-    return launch_attention_cfg(a, 1, 4, 4, s);
+    if (blocks >= 256) return launch_attention_cfg(a, 2, 4, 2, s, ATTN_RUNNING);
+    return launch_attention_cfg(a, 1, 4, 4, s, ATTN_RUNNING);
   }
   dim3 grid((a.T + 63) / 64, a.B * a.H);
   if (a.dh == 64) launch_k(attn_f32_kernel<64>, grid, 64, 0, s, a);

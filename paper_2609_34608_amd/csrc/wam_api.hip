@@ -913,7 +913,7 @@ int wam_set_option(wam_t h, int option, int value) {
       h->use_graphs = value != 0;
       return WAM_OK;
     case WAM_OPT_ATTENTION:
-      if (value < WAM_ATTN_AUTO || value > WAM_ATTN_PINGPONG) return fail(h, WAM_E_ARG, "unknown attention kernel");
+      if (value < WAM_ATTN_AUTO || value > WAM_ATTN_PLAIN) return fail(h, WAM_E_ARG, "unknown attention kernel");
       if (value != h->attn_variant) drop_graphs(h);  // captured launches name the kernel
       h->attn_variant = value;
       return WAM_OK;

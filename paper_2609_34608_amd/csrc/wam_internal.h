@@ -164,10 +164,12 @@ struct AttnArgs {
   int variant;  // WAM_ATTN_*: AUTO picks by shape; bounded forms need bounded set
 };
 hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s);
-// bf16 kernel with qt query tiles of 16 per wave and nw waves per block;
-// bounded selects the fixed-reference kernels (needs a.bounded), nw = 88 the
-// ping-pong form (8 waves in two groups)
-hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int st, hipStream_t s, bool bounded = false);
+// bf16 kernel forms: running max; and with a.bounded, the fixed reference in
+// a software-pipelined loop, a plain loop, or the ping-pong form (8 waves in
+// two groups, nw ignored)
+enum AttnForm : int { ATTN_RUNNING = 0, ATTN_PIPELINED = 1, ATTN_PLAIN = 2, ATTN_PINGPONG = 3 };
+// qt query tiles of 16 per wave, nw waves per block, st K / V^T stages
+hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int st, hipStream_t s, int form = ATTN_RUNNING);
 // Largest score magnitude, log2 units, that the bf16 QKV epilogue can produce
 // for head size 64 with QK-norm gains q_g, k_g (host arrays of 64)
 float attention_score_bound(const float* q_g, const float* k_g);

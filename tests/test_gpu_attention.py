@@ -1,9 +1,9 @@
 """GPU parity of the bf16 attention kernels through the C ABI.
 
-Three kernels exist in bf16 mode: the online softmax with a running max, and
+Four kernels exist in bf16 mode: the online softmax with a running max, and
 (with QK-norm, when the gains bound every score) a fixed softmax reference
-equal to that bound, in a pipelined form and in a ping-pong form whose two
-wave groups alternate MFMA and exp2 phases.  Each must match the float64
+equal to that bound, in a software-pipelined form, a plain loop, and a
+ping-pong form whose two wave groups alternate MFMA and exp2 phases.  Each must match the float64
 oracle at every sequence length class: one key tile, an exact multiple of
 the tile, a one-key tail, and several tiles with a ragged tail.  Tolerance:
 2e-2 (bf16 contractions), max |got-ref| / max |ref|.
@@ -33,7 +33,7 @@ def _spec(Nv, Na, No, L=2):
     return get_workload("small").replace(L=L, D=128, H=2, F=512, Nv=Nv, Na=Na, No=No, B=2)
 
 
-_VARIANTS = ["RUNNING_MAX", "BOUNDED", "PINGPONG"]
+_VARIANTS = ["RUNNING_MAX", "BOUNDED", "PINGPONG", "PLAIN"]
 
 
 @pytest.mark.parametrize("variant", _VARIANTS)
@@ -77,8 +77,9 @@ def test_attention_kernels_agree(dev):
     e = rel_err(outs["BOUNDED"] - h0, outs["RUNNING_MAX"] - h0)
     print(f"bounded vs running-max layer update rel diff {e:.3e}")
     assert e <= 5e-3
-    # the two bounded kernels sum the same bf16 P in the same MFMA order
+    # the bounded kernels sum the same bf16 P in the same MFMA order
     np.testing.assert_array_equal(outs["BOUNDED"], outs["PINGPONG"])
+    np.testing.assert_array_equal(outs["BOUNDED"], outs["PLAIN"])
     m.close()
 
 
@@ -104,3 +105,32 @@ def test_large_gains_fall_back_to_running_max(dev):
     print(f"gains 2.5 x 2.2 velocity rel err {e:.3e}")
     assert e <= BF16_TOL
     m.close()
+
+
+@pytest.mark.parametrize("variant", ["RUNNING_MAX", "BOUNDED", "PINGPONG"])
+def test_large_forced_forms_sampled_rows(dev, variant):
+    """The forms that the automatic choice does not take at the 16-frame
+    shape (T = 10176, 24 heads), run there at their own tile shapes: one
+    layer's update on sampled rows against the oracle."""
+    from paper_2609_34608_amd import _lib as L
+    from gpu_common import model_for
+    spec, W, m = model_for("large", dev)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    k = 3
+    c = OD.cond_vector(W, sig[k])
+    rows = np.unique(np.r_[0, spec.M - 1, spec.T - 1, spec.Nv, spec.Nv + spec.Na,
+                           np.random.default_rng(7).integers(0, spec.M, 10)])
+    m.set_option(L.WAM_OPT_ATTENTION, getattr(L, "WAM_ATTN_" + variant))
+    try:
+        h_in = m.hidden(k, to_dev(x0, dev), to_dev(cond, dev), 0).cpu().numpy()
+        h_out = m.hidden(k, to_dev(x0, dev), to_dev(cond, dev), 1).cpu().numpy().reshape(-1, spec.D)
+    finally:
+        m.set_option(L.WAM_OPT_ATTENTION, L.WAM_ATTN_AUTO)
+    ref = OD.dit_layer_rows(W, spec, 0, h_in, c, rows)
+    h0 = h_in.reshape(-1, spec.D)[rows]
+    e = rel_err(h_out[rows] - h0, ref - h0)
+    print(f"large {variant} layer 0 sampled-row update rel err {e:.3e}")
+    assert e <= BF16_TOL, e
