@@ -306,6 +306,10 @@ __global__ __launch_bounds__(WGM* WGN * 64) void gemm_bf16_kernel(GemmArgs a) {
     __builtin_amdgcn_s_barrier();
     compiler_fence();
     issue(std::integral_constant<int, (j + ST - 1) % ST>{}, min(kt + ST - 1, nk - 1));
+    // the loads must leave before the MFMAs: left to itself the scheduler
+    // sinks them below the compute, next to the wait at the top of the next
+    // step, which exposes their whole latency every stage
+    __builtin_amdgcn_sched_barrier(0);
     compute(J);
   };
 

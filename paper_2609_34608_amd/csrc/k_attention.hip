@@ -280,6 +280,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
     __builtin_amdgcn_s_barrier();
     compiler_fence();
     issue(std::integral_constant<int, (j + ST - 1) % ST>{}, min(kb + ST - 1, nkb - 1));
+    __builtin_amdgcn_sched_barrier(0);  // loads leave before the MFMAs, not sunk below them
     block(J, kb * kKB, MASK, kb == 0);
   };
   const std::integral_constant<bool, false> nomask{};
@@ -469,6 +470,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_bounded_kernel(AttnArgs a) 
     __builtin_amdgcn_s_barrier();
     compiler_fence();
     issue(std::integral_constant<int, (j + ST - 1) % ST>{}, min(kb + ST - 1, nkb - 1));
+    __builtin_amdgcn_sched_barrier(0);  // loads leave before the MFMAs, not sunk below them
     qk(std::integral_constant<int, (j + 1) % ST>{}, std::integral_constant<int, (j + 1) % 2>{});
     pv(std::integral_constant<int, j % ST>{}, std::integral_constant<int, j % 2>{}, kb * kKB, nomask);
   };
@@ -594,6 +596,7 @@ __global__ __launch_bounds__(512) void attn_bf16_pingpong_kernel(AttnArgs a) {
     __builtin_amdgcn_sched_barrier(0);
     compiler_fence();
     issue(m + ST - 2);
+    __builtin_amdgcn_sched_barrier(0);  // loads leave before the phase's MFMAs
   };
   auto sync_odd = [&]() __attribute__((always_inline)) {
     compiler_fence();

@@ -39,6 +39,7 @@ constexpr TileCfg kCfgs[] = {
     {256, 256, 4, 2, 2, 64},  // 21
     {256, 256, 2, 4, 2, 64},  // 22
     {128, 128, 2, 2, 4, 64},  // 23
+    {192, 256, 2, 4, 2, 64},  // 24
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
@@ -74,7 +75,8 @@ hipError_t launch_role(const GemmArgs& a, int cfg, int splits, hipStream_t s) {
     case 20: return launch_c<20, ROLE>(a, splits, s);
     case 21: return launch_c<21, ROLE>(a, splits, s);
     case 22: return launch_c<22, ROLE>(a, splits, s);
-    default: return launch_c<23, ROLE>(a, splits, s);
+    case 23: return launch_c<23, ROLE>(a, splits, s);
+    default: return launch_c<24, ROLE>(a, splits, s);
   }
 }
 
@@ -150,13 +152,19 @@ int gemm_num_configs() { return kNumCfgs; }
 GemmPlan plan_gemm(int M, int N, int K, int epi) {
   // From a sweep of every configuration at the workload shapes.  Large M:
   // 256x256 tiles over 8 waves, K 64 per stage (two stages) for outputs wider
-  // than 1024, K 32 per stage (four stages) otherwise.  Small M (under a few
-  // blocks per CU): 64x64 tiles with K 64 per stage, 64x128 for the QKV
-  // epilogue (whole heads per wave), 128x128 over 8 waves for wide, short-K
-  // outputs; a K split only for grids under half a block per CU.
+  // than 1024, K 32 per stage (four stages) otherwise; 192x256 when 256-row
+  // tiles leave CUs idle (M = 9224, N = 1024: 148 blocks against 196).
+  // Small M (under a few blocks per CU): 64x64 tiles with K 64 per stage,
+  // 64x128 for the QKV epilogue (whole heads per wave), 128x128 over 8 waves
+  // for wide, short-K outputs; a K split only for grids under half a block
+  // per CU.
   GemmPlan p{0, 1};
   if (M >= 2048 && N % 256 == 0) {
-    if (N > 1024 && K % 64 == 0) p.cfg = 22;
+    // under one block per CU with 256-row tiles, 192-row tiles spread the
+    // same work over more CUs as long as they still fit in one round
+    const long cols = N / 256, rows256 = (M + 255) / 256, rows192 = (M + 191) / 192;
+    if (K % 64 == 0 && rows256 * cols < 256 && rows192 * cols <= 256) p.cfg = 24;
+    else if (N > 1024 && K % 64 == 0) p.cfg = 22;
     else p.cfg = N >= 3072 ? 5 : 4;
     return p;
   }
