@@ -178,46 +178,51 @@ __global__ void ln_modulate_kernel(const float* __restrict__ h, const float* __r
 }
 
 // Vectorised form for D % 256 == 0 and bf16 output: lane holds
-// elements 4 lane + 256 i .. +3 (16-byte loads, 8-byte stores).
-constexpr int kMaxV4 = 8;  // D <= 2048
-__global__ void ln_modulate_v4_kernel(const float* __restrict__ h, const float* __restrict__ shift,
-                                      const float* __restrict__ scale, bf16* __restrict__ u, int rows,
-                                      int D, float eps, const int* skip) {
+// elements 4 lane + 256 i .. +3 (16-byte loads, 8-byte stores).  N4 = D / 256
+// is a template argument so that the row and the modulation are fetched by
+// 3 N4 loads issued together, ahead of the reductions (with a run-time count
+// the compiler emitted one load and one wait per chunk).
+template <int N4>
+__global__ __launch_bounds__(256) void ln_modulate_v4_kernel(const float* __restrict__ h, const float* __restrict__ shift,
+                                                             const float* __restrict__ scale, bf16* __restrict__ u,
+                                                             int rows, float eps, const int* skip) {
   if (skip && *skip) return;
+  constexpr int D = N4 * 256;
   const int row = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   if (row >= rows) return;
   const f32x4* hr = reinterpret_cast<const f32x4*>(h + (size_t)row * D);
-  const int n4 = D / 256;
-  f32x4 v[kMaxV4];
+  const f32x4* sc4 = reinterpret_cast<const f32x4*>(scale);
+  const f32x4* sh4 = reinterpret_cast<const f32x4*>(shift);
+  f32x4 v[N4], sc[N4], sh[N4];
+#pragma unroll
+  for (int i = 0; i < N4; ++i) v[i] = hr[lane + kWave * i];
+#pragma unroll
+  for (int i = 0; i < N4; ++i) {
+    sc[i] = sc4[lane + kWave * i];
+    sh[i] = sh4[lane + kWave * i];
+  }
+  __builtin_amdgcn_sched_barrier(0);  // keep the modulation loads ahead of the reductions
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < kMaxV4; ++i)
-    if (i < n4) {
-      v[i] = hr[lane + kWave * i];
-      s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
-    }
+  for (int i = 0; i < N4; ++i) s += (v[i].x + v[i].y) + (v[i].z + v[i].w);
   const float mean = wave_sum(s) / (float)D;
   float q = 0.f;
 #pragma unroll
-  for (int i = 0; i < kMaxV4; ++i)
-    if (i < n4) {
-      const float a = v[i].x - mean, b = v[i].y - mean, c = v[i].z - mean, d = v[i].w - mean;
-      q += (a * a + b * b) + (c * c + d * d);
-    }
+  for (int i = 0; i < N4; ++i) {
+    const float a = v[i].x - mean, b = v[i].y - mean, c = v[i].z - mean, d = v[i].w - mean;
+    q += (a * a + b * b) + (c * c + d * d);
+  }
   const float rstd = rsqrtf(wave_sum(q) / (float)D + eps);
 #pragma unroll
-  for (int i = 0; i < kMaxV4; ++i)
-    if (i < n4) {
-      const int c = 4 * (lane + kWave * i);
-      const float4 sc = *reinterpret_cast<const float4*>(scale + c);
-      const float4 sh = *reinterpret_cast<const float4*>(shift + c);
-      bf16x4 o = {static_cast<bf16>((v[i].x - mean) * rstd * (1.0f + sc.x) + sh.x),
-                  static_cast<bf16>((v[i].y - mean) * rstd * (1.0f + sc.y) + sh.y),
-                  static_cast<bf16>((v[i].z - mean) * rstd * (1.0f + sc.z) + sh.z),
-                  static_cast<bf16>((v[i].w - mean) * rstd * (1.0f + sc.w) + sh.w)};
-      *reinterpret_cast<bf16x4*>(u + (size_t)row * D + c) = o;
-    }
+  for (int i = 0; i < N4; ++i) {
+    const int c = 4 * (lane + kWave * i);
+    bf16x4 o = {static_cast<bf16>((v[i].x - mean) * rstd * (1.0f + sc[i].x) + sh[i].x),
+                static_cast<bf16>((v[i].y - mean) * rstd * (1.0f + sc[i].y) + sh[i].y),
+                static_cast<bf16>((v[i].z - mean) * rstd * (1.0f + sc[i].z) + sh[i].z),
+                static_cast<bf16>((v[i].w - mean) * rstd * (1.0f + sc[i].w) + sh[i].w)};
+    *reinterpret_cast<bf16x4*>(u + (size_t)row * D + c) = o;
+  }
 }
 
 // ------------------------------------------------------------- final layer + Euler
@@ -800,9 +805,18 @@ hipError_t launch_ln_modulate(const float* h, const float* shift, const float* s
   if (D % kWave || D / kWave > kMaxVpl) return hipErrorInvalidValue;
   const int wpb = 4;
   dim3 grid((rows + wpb - 1) / wpb);
-  if (bf16_out && D % 256 == 0)
-    launch_k(ln_modulate_v4_kernel, grid, wpb * kWave, 0, s, h, shift, scale, (bf16*)u, rows, D, eps, skip);
-  else if (bf16_out)
+  if (bf16_out && D % 256 == 0 && D <= 2048) {
+    switch (D / 256) {
+      case 1: launch_k(ln_modulate_v4_kernel<1>, grid, wpb * kWave, 0, s, h, shift, scale, (bf16*)u, rows, eps, skip); break;
+      case 2: launch_k(ln_modulate_v4_kernel<2>, grid, wpb * kWave, 0, s, h, shift, scale, (bf16*)u, rows, eps, skip); break;
+      case 3: launch_k(ln_modulate_v4_kernel<3>, grid, wpb * kWave, 0, s, h, shift, scale, (bf16*)u, rows, eps, skip); break;
+      case 4: launch_k(ln_modulate_v4_kernel<4>, grid, wpb * kWave, 0, s, h, shift, scale, (bf16*)u, rows, eps, skip); break;
+      case 5: launch_k(ln_modulate_v4_kernel<5>, grid, wpb * kWave, 0, s, h, shift, scale, (bf16*)u, rows, eps, skip); break;
+      case 6: launch_k(ln_modulate_v4_kernel<6>, grid, wpb * kWave, 0, s, h, shift, scale, (bf16*)u, rows, eps, skip); break;
+      case 7: launch_k(ln_modulate_v4_kernel<7>, grid, wpb * kWave, 0, s, h, shift, scale, (bf16*)u, rows, eps, skip); break;
+      default: launch_k(ln_modulate_v4_kernel<8>, grid, wpb * kWave, 0, s, h, shift, scale, (bf16*)u, rows, eps, skip); break;
+    }
+  } else if (bf16_out)
     launch_k(ln_modulate_kernel<bf16>, grid, wpb * kWave, 0, s, h, shift, scale, (bf16*)u, rows, D, eps, skip);
   else
     launch_k(ln_modulate_kernel<float>, grid, wpb * kWave, 0, s, h, shift, scale, (float*)u, rows, D, eps, skip);
