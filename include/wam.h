@@ -110,7 +110,9 @@ extern "C" {
 #define WAM_ATTN_PINGPONG 3       /* bounded, 8 waves in two groups that alternate
                                      MFMA and exp2 phases on each SIMD            */
 #define WAM_ATTN_PLAIN 4          /* bounded, plain loop (one score buffer, more
-                                     waves per SIMD)                              */
+                                     waves per SIMD); on grids too small to fill
+                                     the chip, two wave groups split the keys and
+                                     add their partial sums                      */
 /* A bounded form asked for on a layer whose gains allow no bound (mref > 60)
    runs the running-max kernel. */
 

@@ -105,22 +105,33 @@ __device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory")
 // BND: the fixed reference of the bounded kernels (a.mref) instead of the
 // running max, in this plain (not software-pipelined) loop, which needs one
 // score buffer and so leaves room for more waves per SIMD.
-template <int QT, int NW, int ST, bool BND = false>
-__global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
+// KSPLIT > 1 (bounded only): KSPLIT groups of NW waves take the same queries
+// and split the keys, group g taking key tiles g, g + KSPLIT, ...  With a
+// fixed reference the partial O and l of the groups simply add (no
+// rescaling), which group 0 does at the end through LDS, in group order.
+// This shortens the serial chain of key tiles per wave where the grid is too
+// small to fill the chip (short sequences).
+template <int QT, int NW, int ST, bool BND = false, int KSPLIT = 1>
+__global__ __launch_bounds__(NW * KSPLIT * 64) void attn_bf16_kernel(AttnArgs a) {
   constexpr int QB = NW * QT * 16;  // queries per block
-  constexpr int NI = 16;            // 1 KiB load instructions per stage: K rows 0-63, V^T rows 64-127
-  constexpr int IPW = NI / NW;
-  static_assert(IPW >= 1 && IPW * NW == NI, "stage load split");
+  constexpr int NWT = NW * KSPLIT;  // waves per block
+  // 1 KiB load instructions per stage: per key tile K rows 0-63, V^T rows 64-127
+  constexpr int NI = 16 * KSPLIT;
+  constexpr int IPW = NI / NWT;
+  static_assert(IPW >= 1 && IPW * NWT == NI, "stage load split");
   static_assert(ST >= 2 && (ST - 2) * IPW < 64, "stage count");
+  static_assert(KSPLIT == 1 || BND, "key split needs the fixed reference");
   if (a.skip && *a.skip) return;
-  // stage: 128 rows of 64 bf16 (128 bytes); chunk c of row r stored at c ^ (r & 7)
-  __shared__ __attribute__((aligned(1024))) bf16 sm[ST][128 * kDh];
+  // stage: KSPLIT key tiles of 128 rows of 64 bf16 (128 bytes); chunk c of
+  // row r stored at c ^ (r & 7)
+  __shared__ __attribute__((aligned(1024))) bf16 sm[ST][KSPLIT * 128 * kDh];
 
   int qb, bh;
   attn_block(qb, bh);
   const int b = bh / a.H, h = bh % a.H;
   const int tid = threadIdx.x, lane = tid % 64, wid = tid / 64;
-  const int q0 = qb * QB + wid * QT * 16;
+  const int kgrp = wid / NW, wl = wid % NW;
+  const int q0 = qb * QB + wl * QT * 16;
   const int g = lane / 16, lr = lane % 16;
 
   const bf16* Q = static_cast<const bf16*>(a.q) + (size_t)bh * a.Tpad * kDh;
@@ -153,30 +164,40 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
   for (int i = 0; i < 8; ++i) ones[i] = static_cast<bf16>(1.0f);
 
   // Load instruction j of this wave fills stage rows 8*i .. 8*i+7 with
-  // i = wid + NW*j; lane l writes chunk l%8 of row l/8, i.e. global chunk
-  // (l%8) ^ (row & 7).  Rows 0-63 are keys (K rows), rows 64-127 are dh rows
-  // of V^T; the next key tile is 64 K rows or 64 V^T columns further on.
+  // i = wid + NWT*j; lane l writes chunk l%8 of row l/8, i.e. global chunk
+  // (l%8) ^ (row & 7).  Stage rows 128u .. 128u+127 hold key tile u of the
+  // stage's KSPLIT tiles: rows 0-63 are keys (K rows), rows 64-127 are dh
+  // rows of V^T; the next key tile is 64 K rows or 64 V^T columns further on.
   const bf16* src[IPW];
+  int sub[IPW];
 #pragma unroll
   for (int j = 0; j < IPW; ++j) {
-    const int row = 8 * (wid + NW * j) + lane / 8;
+    const int i = wid + NWT * j;
+    const int row = 8 * (i % 16) + lane / 8;
     const int col = ((lane % 8) ^ (row & 7)) * 8;
-    src[j] = j < IPW / 2 ? Kg + (size_t)row * kDh + col : Vg + (size_t)(row - 64) * a.Tpad + col;
+    sub[j] = i / 16;
+    src[j] = row < 64 ? Kg + (size_t)row * kDh + col : Vg + (size_t)(row - 64) * a.Tpad + col;
   }
-  auto issue = [&](auto S, int kb) __attribute__((always_inline)) {
+  const int nkb = a.Tpad / kKB;
+  // stage kp holds key tiles KSPLIT kp + u (past the last tile: the last tile
+  // again, into rows nobody reads)
+  auto issue = [&](auto S, int kp) __attribute__((always_inline)) {
     constexpr int s = decltype(S)::value;
 #pragma unroll
     for (int j = 0; j < IPW; ++j) {
-      // instructions 0-7 of a stage (j < IPW/2 for every wave) carry K rows
-      const size_t step = j < IPW / 2 ? (size_t)kKB * kDh : (size_t)kKB;
+      const int i = wid + NWT * j;
+      // one tile per stage: instructions j < IPW/2 carry K rows for every wave
+      const bool krow = KSPLIT == 1 ? j < IPW / 2 : (i % 16) < 8;
+      const int kb = KSPLIT == 1 ? kp : min(kp * KSPLIT + sub[j], nkb - 1);
+      const size_t step = krow ? (size_t)kKB * kDh : (size_t)kKB;
       __builtin_amdgcn_global_load_lds((const global_void*)(src[j] + kb * step),
-                                       (lds_void*)(&sm[s][(wid + NW * j) * 512]), 16, 0, 0);
+                                       (lds_void*)(&sm[s][i * 512]), 16, 0, 0);
     }
   };
 
   const int sw = lr & 7;  // swizzle of every row this lane reads (tile rows are multiples of 16)
   auto block = [&](auto S, int k0, auto MASK, bool first) __attribute__((always_inline)) {
-    const bf16* st = sm[decltype(S)::value];
+    const bf16* st = sm[decltype(S)::value] + (KSPLIT > 1 ? kgrp * 128 * kDh : 0);
     // S^T - m tiles [key tile kt][query tile qt]: the accumulators start at -m
     f32x4 s[4][QT];
 #pragma unroll
@@ -268,36 +289,73 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
     }
   };
 
-  // one key tile on stage slot J: this wave's loads of tile kb have landed and
-  // its LDS reads are done; after the barrier everyone's are, and the slot of
-  // the previous tile takes tile kb+ST-1 (past the end the last tile again,
-  // into slots nobody reads, which keeps the wait counts uniform)
-  const int nkb = a.Tpad / kKB;
-  auto step = [&](auto J, int kb, auto MASK) __attribute__((always_inline)) {
+  // one stage (KSPLIT key tiles) on slot J: this wave's loads of stage kp
+  // have landed and its LDS reads are done; after the barrier everyone's are,
+  // and the slot of the previous stage takes stage kp+ST-1 (past the end the
+  // last stage again, into slots nobody reads, which keeps the wait counts
+  // uniform).  Group kgrp works on key tile KSPLIT kp + kgrp.
+  const int nkp = (nkb + KSPLIT - 1) / KSPLIT;
+  const std::integral_constant<bool, false> nomask{};
+  const std::integral_constant<bool, true> withmask{};
+  auto step = [&](auto J, int kp, auto TAIL) __attribute__((always_inline)) {
     constexpr int j = decltype(J)::value;
     __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0((ST - 2) * IPW));
     compiler_fence();
     __builtin_amdgcn_s_barrier();
     compiler_fence();
-    issue(std::integral_constant<int, (j + ST - 1) % ST>{}, min(kb + ST - 1, nkb - 1));
+    issue(std::integral_constant<int, (j + ST - 1) % ST>{}, min(kp + ST - 1, nkp - 1));
     __builtin_amdgcn_sched_barrier(0);  // loads leave before the MFMAs, not sunk below them
-    block(J, kb * kKB, MASK, kb == 0);
+    const int kb = kp * KSPLIT + kgrp;
+    if constexpr (!decltype(TAIL)::value) {
+      block(J, kb * kKB, nomask, kb == 0);
+    } else {
+      // the last stage: the last key tile carries the padded keys, and with
+      // a key split some group may have no tile left
+      if (kb < nkb - 1) block(J, kb * kKB, nomask, kb == 0);
+      else if (kb == nkb - 1) block(J, kb * kKB, withmask, kb == 0);
+    }
   };
-  const std::integral_constant<bool, false> nomask{};
-  const std::integral_constant<bool, true> withmask{};
-  static_for<ST - 1>([&](auto P) __attribute__((always_inline)) { issue(P, min((int)decltype(P)::value, nkb - 1)); });
-  // tiles 0 .. nkb-2 carry no padded keys; the last one runs with the mask
-  const int nbody = nkb - 1;
+  static_for<ST - 1>([&](auto P) __attribute__((always_inline)) { issue(P, min((int)decltype(P)::value, nkp - 1)); });
+  // stages 0 .. nkp-2 carry no padded keys; the last one runs as the tail
+  const int nbody = nkp - 1;
   const int nfull = nbody / ST * ST;
-  for (int kb0 = 0; kb0 < nfull; kb0 += ST)
-    static_for<ST>([&](auto J) __attribute__((always_inline)) { step(J, kb0 + decltype(J)::value, nomask); });
+  for (int kp0 = 0; kp0 < nfull; kp0 += ST)
+    static_for<ST>([&](auto J) __attribute__((always_inline)) { step(J, kp0 + decltype(J)::value, nomask); });
   static_for<ST>([&](auto J) __attribute__((always_inline)) {
-    const int kb = nfull + decltype(J)::value;
-    if (kb < nbody) step(J, kb, nomask);
-    else if (kb == nbody) step(J, kb, withmask);
+    const int kp = nfull + decltype(J)::value;
+    if (kp < nbody) step(J, kp, nomask);
+    else if (kp == nbody) step(J, kp, withmask);
   });
   // no load may still be writing this block's LDS when the block retires
   __builtin_amdgcn_s_waitcnt(0);
+
+  if constexpr (KSPLIT > 1) {
+    // groups 1.. hand O and l to group 0 through the idle stages
+    static_assert((KSPLIT - 1) * NW * 5 * QT * 64 * 16 <= ST * KSPLIT * 128 * kDh * 2, "LDS for the key-split sum");
+    f32x4* xch = reinterpret_cast<f32x4*>(&sm[0][0]);
+    __syncthreads();
+    if (kgrp > 0) {
+      f32x4* w = xch + ((kgrp - 1) * NW + wl) * 5 * QT * 64 + lane;
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) w[(qt * 5 + d) * 64] = o[d][qt];
+        w[(qt * 5 + 4) * 64] = l[qt];
+      }
+    }
+    __syncthreads();
+    if (kgrp > 0) return;
+#pragma unroll
+    for (int g2 = 1; g2 < KSPLIT; ++g2) {
+      const f32x4* w = xch + ((g2 - 1) * NW + wl) * 5 * QT * 64 + lane;
+#pragma unroll
+      for (int qt = 0; qt < QT; ++qt) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) o[d][qt] += w[(qt * 5 + d) * 64];
+        l[qt] += w[(qt * 5 + 4) * 64];
+      }
+    }
+  }
 
   // normalise and store O[b*T + q][h*64 + dh]; lane holds dh = d*16 + 4g + r of query lr
   bf16* out = static_cast<bf16*>(a.out);
@@ -795,12 +853,17 @@ hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int st, hipSt
         default: return hipErrorInvalidValue;
       }
       break;
+    case ATTN_PLAIN_KSPLIT:
+      switch (key) {
+        case 10402: launch_k(attn_bf16_kernel<1, 4, 2, true, 2>, grid, 512, 0, s, a); break;
+        default: return hipErrorInvalidValue;
+      }
+      break;
     case ATTN_PLAIN:
       switch (key) {
         case 20402: launch_k(attn_bf16_kernel<2, 4, 2, true>, grid, 256, 0, s, a); break;
         case 20403: launch_k(attn_bf16_kernel<2, 4, 3, true>, grid, 256, 0, s, a); break;
         case 40802: launch_k(attn_bf16_kernel<4, 8, 2, true>, grid, 512, 0, s, a); break;
-        case 10402: launch_k(attn_bf16_kernel<1, 4, 2, true>, grid, 256, 0, s, a); break;
         default: return hipErrorInvalidValue;
       }
       break;
@@ -844,15 +907,16 @@ hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s) {
     if (a.variant == WAM_ATTN_PINGPONG) return launch_attention_cfg(a, 4, 8, 4, s, ATTN_PINGPONG);
     // from a sweep at the workload shapes: long sequences with about two
     // blocks of 512 queries per CU take 8 waves of 64 queries; 4 waves of 32
-    // queries when that fills the chip; short grids 4 waves of 16 queries,
-    // where the pipelined loop hides the most latency
+    // queries when that fills the chip; short grids (T = 864, 12 heads: 168
+    // blocks) two groups of 4 waves of 16 queries that split the keys (8.5
+    // against 9.3 us), unless there are too few key tiles to split
     const bool big = a.T >= 4096 && (long)((a.T + 511) / 512) * a.B * a.H >= 384;
     const bool full = (long)((a.T + 127) / 128) * a.B * a.H >= 256;
     if (a.variant == WAM_ATTN_BOUNDED)
       return full ? launch_attention_cfg(a, 2, 4, 4, s, ATTN_PIPELINED) : launch_attention_cfg(a, 1, 4, 4, s, ATTN_PIPELINED);
     if (big) return launch_attention_cfg(a, 4, 8, 2, s, ATTN_PLAIN);
     if (full) return launch_attention_cfg(a, 2, 4, 2, s, ATTN_PLAIN);
-    if (a.variant == WAM_ATTN_PLAIN) return launch_attention_cfg(a, 1, 4, 2, s, ATTN_PLAIN);
+    if (a.variant == WAM_ATTN_PLAIN || a.Tpad / kKB >= 4) return launch_attention_cfg(a, 1, 4, 2, s, ATTN_PLAIN_KSPLIT);
     return launch_attention_cfg(a, 1, 4, 4, s, ATTN_PIPELINED);
   }
   if (bf16_mode) {

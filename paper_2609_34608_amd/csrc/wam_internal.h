@@ -165,9 +165,10 @@ struct AttnArgs {
 };
 hipError_t launch_attention(const AttnArgs& a, bool bf16_mode, hipStream_t s);
 // bf16 kernel forms: running max; and with a.bounded, the fixed reference in
-// a software-pipelined loop, a plain loop, or the ping-pong form (8 waves in
-// two groups, nw ignored)
-enum AttnForm : int { ATTN_RUNNING = 0, ATTN_PIPELINED = 1, ATTN_PLAIN = 2, ATTN_PINGPONG = 3 };
+// a software-pipelined loop, a plain loop (also with two wave groups that
+// split the keys: 2 nw waves), or the ping-pong form (8 waves in two groups,
+// nw ignored)
+enum AttnForm : int { ATTN_RUNNING = 0, ATTN_PIPELINED = 1, ATTN_PLAIN = 2, ATTN_PINGPONG = 3, ATTN_PLAIN_KSPLIT = 4 };
 // qt query tiles of 16 per wave, nw waves per block, st K / V^T stages
 hipError_t launch_attention_cfg(const AttnArgs& a, int qt, int nw, int st, hipStream_t s, int form = ATTN_RUNNING);
 // Largest score magnitude, log2 units, that the bf16 QKV epilogue can produce

@@ -2,8 +2,10 @@
 
 Four kernels exist in bf16 mode: the online softmax with a running max, and
 (with QK-norm, when the gains bound every score) a fixed softmax reference
-equal to that bound, in a software-pipelined form, a plain loop, and a
-ping-pong form whose two wave groups alternate MFMA and exp2 phases.  Each must match the float64
+equal to that bound, in a software-pipelined form, a plain loop (on these
+short grids with the keys split over two wave groups, including groups left
+without a key tile), and a ping-pong form whose two wave groups alternate
+MFMA and exp2 phases.  Each must match the float64
 oracle at every sequence length class: one key tile, an exact multiple of
 the tile, a one-key tail, and several tiles with a ragged tail.  Tolerance:
 2e-2 (bf16 contractions), max |got-ref| / max |ref|.
@@ -77,9 +79,14 @@ def test_attention_kernels_agree(dev):
     e = rel_err(outs["BOUNDED"] - h0, outs["RUNNING_MAX"] - h0)
     print(f"bounded vs running-max layer update rel diff {e:.3e}")
     assert e <= 5e-3
-    # the bounded kernels sum the same bf16 P in the same MFMA order
+    # the pipelined and ping-pong kernels sum the same bf16 P in the same
+    # MFMA order; the plain form splits the keys of this short grid over two
+    # wave groups, whose partial sums differ from the single sum by fp32
+    # rounding only
     np.testing.assert_array_equal(outs["BOUNDED"], outs["PINGPONG"])
-    np.testing.assert_array_equal(outs["BOUNDED"], outs["PLAIN"])
+    e2 = rel_err(outs["PLAIN"] - h0, outs["BOUNDED"] - h0)
+    print(f"key-split vs single-group layer update rel diff {e2:.3e}")
+    assert e2 <= 1e-3
     m.close()
 
 
