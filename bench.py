@@ -612,6 +612,8 @@ def ablation(args):
                        "or_accept": n_bind / n_start if n_start else None,
                        "or_coverage": n_bind / len(infos),
                        "rr_accept": sum(i.rr_reuses for i in infos) / att if att else None}
+        print(f"ablation {name}: {table[name]['gpu_ms']:.3f} ms GPU, {table[name]['o2a_ms']:.3f} ms O2A",
+              file=sys.stderr, flush=True)
     base = table["native"]
     for v in table.values():
         v["gpu_speedup"] = round(base["gpu_ms"] / v["gpu_ms"], 3)

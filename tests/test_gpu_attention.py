@@ -141,3 +141,28 @@ def test_large_forced_forms_sampled_rows(dev, variant):
     e = rel_err(h_out[rows] - h0, ref - h0)
     print(f"large {variant} layer 0 sampled-row update rel err {e:.3e}")
     assert e <= BF16_TOL, e
+
+
+@pytest.mark.parametrize("shape", [dict(Nv=0, Na=16, No=8), dict(Nv=40, Na=16, No=0), dict(Nv=24, Na=1, No=3),
+                                   dict(Nv=24, Na=8, No=3, B=16), dict(Nv=63, Na=16, No=1)])
+def test_bf16_degenerate_shapes_match_oracle(dev, shape):
+    """The bf16 path (GEMM planner, attention forms, final heads) on the
+    degenerate shapes: no video tokens, no observation tokens, a one-slot
+    action chunk, the maximum batch, and a ragged sequence; the velocity of
+    two steps within the bf16 tolerance."""
+    from paper_2609_34608_amd import runtime as R
+    B = shape.pop("B", 2)
+    spec = _spec(**shape).replace(B=B)
+    W = make_weights(spec, bias_std=0.02, gain_std=0.1)
+    m = R.WamModel(R.config_of(spec), W, device=dev)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    for k in (0, 5):
+        v, _ = m.velocity(k, to_dev(x0, dev), to_dev(cond, dev))
+        ref = OD.velocity(W, spec, x0, cond, sig[k])
+        e = rel_err(v.cpu().numpy(), ref)
+        print(f"{shape} B={B} T={spec.T} step {k} velocity rel err {e:.3e}")
+        assert e <= BF16_TOL, (k, e)
+    m.close()
