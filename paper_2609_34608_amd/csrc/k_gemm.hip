@@ -40,6 +40,7 @@ constexpr TileCfg kCfgs[] = {
     {256, 256, 2, 4, 2, 64},  // 22
     {128, 128, 2, 2, 4, 64},  // 23
     {192, 256, 2, 4, 2, 64},  // 24
+    {320, 256, 2, 4, 2, 64},  // 25
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
@@ -76,7 +77,8 @@ hipError_t launch_role(const GemmArgs& a, int cfg, int splits, hipStream_t s) {
     case 21: return launch_c<21, ROLE>(a, splits, s);
     case 22: return launch_c<22, ROLE>(a, splits, s);
     case 23: return launch_c<23, ROLE>(a, splits, s);
-    default: return launch_c<24, ROLE>(a, splits, s);
+    case 24: return launch_c<24, ROLE>(a, splits, s);
+    default: return launch_c<25, ROLE>(a, splits, s);
   }
 }
 
@@ -151,20 +153,37 @@ int gemm_num_configs() { return kNumCfgs; }
 
 GemmPlan plan_gemm(int M, int N, int K, int epi) {
   // From a sweep of every configuration at the workload shapes.  Large M:
-  // 256x256 tiles over 8 waves, K 64 per stage (two stages) for outputs wider
-  // than 1024, K 32 per stage (four stages) otherwise; 192x256 when 256-row
-  // tiles leave CUs idle (M = 9224, N = 1024: 148 blocks against 196).
-  // Small M (under a few blocks per CU): 64x64 tiles with K 64 per stage,
-  // 64x128 for the QKV epilogue (whole heads per wave), 128x128 over 8 waves
-  // for wide, short-K outputs; a K split only for grids under half a block
-  // per CU.
+  // tiles of 256 columns over 8 waves, K 64 per stage (two stages), with the
+  // row count (192, 256 or 320) that minimises whole rounds of one block per
+  // CU times rows per block, weighted by the per-row cost each tile height
+  // measured (192-row tiles ~10% dearer per row, 320-row ~3% cheaper).  For
+  // example M = 9224, N = 4096 (mid MLP-up): 592 blocks of 256 rows take 3
+  // rounds, 464 of 320 rows take 2 (98 -> 82 us); M = 9224, N = 1024: 196
+  // blocks of 192 rows fill one round that 148 of 256 leave a third idle
+  // (97 -> 83 us).  256 rows with K 32 per stage (four stages) for outputs of
+  // 1024 columns or fewer, or K not a multiple of 64.  Small M (under a few
+  // blocks per CU): 64x64 tiles with K 64 per stage, 64x128 for the QKV
+  // epilogue (whole heads per wave), 128x128 over 8 waves for wide, short-K
+  // outputs; a K split only for grids under half a block per CU.
   GemmPlan p{0, 1};
   if (M >= 2048 && N % 256 == 0) {
-    // under one block per CU with 256-row tiles, 192-row tiles spread the
-    // same work over more CUs as long as they still fit in one round
-    const long cols = N / 256, rows256 = (M + 255) / 256, rows192 = (M + 191) / 192;
-    if (K % 64 == 0 && rows256 * cols < 256 && rows192 * cols <= 256) p.cfg = 24;
-    else if (N > 1024 && K % 64 == 0) p.cfg = 22;
+    if (K % 64 == 0) {
+      const long cols = N / 256;
+      auto cost = [&](int bm, double per_row) {
+        const long blocks = (M + bm - 1) / bm * cols;
+        return (double)((blocks + 255) / 256) * bm * per_row;
+      };
+      const double c192 = cost(192, 1.10), c256 = cost(256, 1.0), c320 = cost(320, 0.97);
+      if (c192 < c256 && c192 <= c320) {
+        p.cfg = 24;
+        return p;
+      }
+      if (c320 < c256) {
+        p.cfg = 25;
+        return p;
+      }
+    }
+    if (N > 1024 && K % 64 == 0) p.cfg = 22;
     else p.cfg = N >= 3072 ? 5 : 4;
     return p;
   }
