@@ -139,6 +139,9 @@ def parse():
     p.add_argument("--pmc-command", action="append", default=[], help="command lines recorded in the summary")
     p.add_argument("--ablation", action="store_true",
                    help="closed-loop GPU time and observation-to-action latency per variant, then exit")
+    p.add_argument("--diagnostics", action="store_true",
+                   help="state-continuity diagnostics (layer change, reuse output error, consecutive-replan "
+                        "latent similarity, remapped-vs-native action RMSE), then exit")
     p.add_argument("--window-ms", type=float, default=20.0,
                    help="simulated action-execution window between replans (ablation mode)")
     return p.parse_args()
@@ -158,6 +161,9 @@ def main():
             print("the ablation runs on the single-model workloads", file=sys.stderr)
             sys.exit(2)
         ablation(args)
+        return
+    if args.diagnostics:
+        diagnostics(args)
         return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); multi-GPU runs are not part "
@@ -621,6 +627,116 @@ def ablation(args):
     print(json.dumps({"workload": spec.name, "window_ms": args.window_ms, "replans": args.steps,
                       "variants": table}), flush=True)
     m.close()
+
+
+def rel_l2(a, ref) -> float:
+    """||a - ref|| / ||ref|| in float64 (device tensors)."""
+    a, ref = a.double(), ref.double()
+    return float((a - ref).norm() / ref.norm())
+
+
+def layer_diagnostics(m, spec, x0, cond, rr_force, n_steps):
+    """Layer-state diagnostics along the native trajectory from x0 under cond
+    (Eq. app-layer-errors): at step i, Delta_l(i) = ||h_{l+1} - h_l|| / ||h_l||
+    for every layer l, and E_out(i) = ||y_reuse - y_full|| / ||y_full||, the
+    output of the residual-reuse path (reuse forced, retained state from the
+    previous step) against full computation on the same input.  Returns
+    (delta [n_steps][L], e_out [n_steps]); step 0 only establishes the
+    retained state, so its E_out is that of a full evaluation (0)."""
+    x = x0.clone()
+    m.reset_layer_state()
+    delta, e_out = [], []
+    for i in range(n_steps):
+        hs = [m.hidden(i, x, cond, n) for n in range(spec.L + 1)]
+        delta.append([rel_l2(hs[l + 1], hs[l]) for l in range(spec.L)])
+        v_full, _ = m.velocity(i, x, cond)
+        v_reuse, _ = m.velocity(i, x, cond, rr=rr_force)
+        e_out.append(rel_l2(v_reuse, v_full))
+        m.denoise_step(i, x, cond)
+    return delta, e_out
+
+
+def action_part(spec, x):
+    """[B, Na, A] action slots of trajectories [B, traj] (video first)."""
+    return x[:, spec.Nv * spec.Cv:].reshape(x.shape[0], spec.Na, spec.A)
+
+
+def diagnostics(args):
+    """State-continuity diagnostics of the paper's analysis protocols on the
+    synthetic model: layer change and reuse output error along a native
+    trajectory; cos and relative L2 of the retained latent x^r between
+    consecutive closed-loop replans (Eq. app-trajectory-similarity); action
+    RMSE of remapped inference (K - b0 steps, OR and RR off) against native
+    inference (K steps) under the same observation and initial noise, both
+    continuing from the native replan of the previous observation (Eq.
+    app-action-rmse)."""
+    import numpy as np
+    import torch
+
+    from paper_2609_34608_amd import _lib as L
+    from paper_2609_34608_amd import runtime as R
+    from synth import get_workload, make_weights, make_initial_noise, make_observations, make_remap_noise
+
+    spec = get_workload(args.workload)
+    dev = torch.device("cuda:0")
+    W = make_weights(spec)
+    m = R.WamModel(R.config_of(spec), W, device=dev)
+    K = spec.K
+    m.set_schedule(1.0 - np.arange(K + 1) / K)
+    q, s_, e = spec.rr_bounds
+    rr_kw = (spec.rr_alpha_min, spec.rr_alpha_max, spec.rr_eps, spec.rr_gamma_cos, spec.rr_gamma_fit)
+    rr_auto = R.rr_profile(q, s_, e, L.WAM_RR_AUTO, *rr_kw)
+    rr_force = R.rr_profile(q, s_, e, L.WAM_RR_FORCE_SKIP, *rr_kw)
+    n = max(3, min(args.steps, 8))
+    obs = make_observations(spec, n + 1)
+    rho = spec.ar_rho
+    delta_or = 1.0 / np.sqrt(1.0 - rho * rho)
+    obs_d = torch.from_numpy(obs).to(dev)
+    pred_d = torch.from_numpy((rho * obs[:-1]).astype(np.float32)).to(dev)
+    noise_first = torch.from_numpy(make_initial_noise(spec)).to(dev)
+    remap_noise = torch.from_numpy(np.stack([make_remap_noise(spec, t) for t in range(n + 1)])).to(dev)
+    ra = dict(b0=spec.tr_b0, r=spec.tr_r, shift_action=spec.shift_action, shift_video=spec.shift_video,
+              k1=spec.or_k1, tau=spec.or_tau, kappa_max=spec.or_kappa_max)
+
+    delta, e_out = layer_diagnostics(m, spec, noise_first, obs_d[0], rr_force, K)
+    print(f"diagnostics: layer change and output error over {K} steps", file=sys.stderr, flush=True)
+
+    # consecutive closed-loop replans (TR + OR + RR as in the replay workload)
+    m.reset_all()
+    x_out = m.new_traj()
+    cos_r, rel_r, prev = [], [], None
+    for t in range(n):
+        cp = pred_d[t - 1] if t > 0 else obs_d[t]
+        m.replan(obs_d[t], x_out, remap_noise[t], cond_pred=cp, u_hat=[cp], u=[obs_d[t]], delta=[delta_or],
+                 weight=[1.0], noise_first=noise_first, rr=rr_auto, **ra)
+        _, xr, _ = m.get_replan_state()
+        if prev is not None:
+            a, b = xr.double().flatten(), prev.double().flatten()
+            cos_r.append(float(a.dot(b) / (a.norm() * b.norm())))
+            rel_r.append(rel_l2(xr, prev))
+        prev = xr.clone()
+    print(f"diagnostics: {n} consecutive replans", file=sys.stderr, flush=True)
+
+    # remapped (K - b0 steps) against native (K steps), OR and RR off
+    rmse, x_tr, x_nat = [], m.new_traj(), m.new_traj()
+    for t in range(1, n):
+        m.reset_all()  # the next replan is native (K steps from noise) and leaves the replan state
+        m.replan(obs_d[t - 1], x_nat, remap_noise[t - 1], noise_first=noise_first, or_enabled=False, **ra)
+        m.replan(obs_d[t], x_tr, remap_noise[t], noise_first=noise_first, or_enabled=False, **ra)
+        m.reset_all()
+        m.replan(obs_d[t], x_nat, remap_noise[t], noise_first=noise_first, or_enabled=False, **ra)
+        d = action_part(spec, x_tr).double() - action_part(spec, x_nat).double()
+        rmse.append(float(d.pow(2).mean().sqrt()))
+    m.close()
+    out = {"diagnostics": spec.name, "data": "synthetic (seeded random-init weights)",
+           "layer_change_mean": [round(float(v), 6) for v in np.mean(delta, axis=0)],
+           "layer_change_per_step": [[round(v, 6) for v in row] for row in delta],
+           "output_error_reuse_vs_full": [round(v, 6) for v in e_out],
+           "replan_latent_cos": [round(v, 6) for v in cos_r],
+           "replan_latent_rel_l2": [round(v, 6) for v in rel_r],
+           "action_rmse_remapped_vs_native": [round(v, 6) for v in rmse],
+           "protocol": {"steps": K, "replans": n, "remapped_steps": K - spec.tr_b0, "native_steps": K}}
+    print(json.dumps(out), flush=True)
 
 
 def cpu_baseline(spec, W, obs, n_steps, single=False):
