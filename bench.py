@@ -9,7 +9,7 @@ Residual Rescaling inside every denoising step, all through libwam.  Inputs
 (weights, noise, AR(1) observations) are seeded, synthetic and resident in HBM
 before timing starts.
 
-Prints one JSON line.  --gpus N > 1 is refused: this build runs on one GPU.
+Prints one JSON line.  --gpus N > 1 is refused: the library runs on one GPU.
 """
 from __future__ import annotations
 
@@ -166,8 +166,8 @@ def main():
         diagnostics(args)
         return
     if args.gpus != 1:
-        print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); multi-GPU runs are not part "
-              "of this build.", file=sys.stderr)
+        print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); the library has no "
+              "multi-GPU path.", file=sys.stderr)
         sys.exit(2)
     from synth.workloads import PAIRS
     if args.workload in PAIRS:
