@@ -56,7 +56,7 @@ extern "C" {
 #define WAM_E_STATE (-3)       /* call not valid in the handle's state        */
 #define WAM_E_HIP (-4)         /* HIP runtime error                           */
 #define WAM_E_WORKSPACE (-5)   /* weight or workspace buffer too small        */
-#define WAM_E_UNSUPPORTED (-6) /* valid request this build does not implement */
+#define WAM_E_UNSUPPORTED (-6) /* valid request the library does not implement */
 
 /* ---- numeric modes --------------------------------------------------- */
 #define WAM_FP32 0 /* all activations and contractions in float32            */
