@@ -138,6 +138,44 @@ __global__ void embed_kernel(EmbedArgs a) {
   }
 }
 
+// Vectorised form: one block per token row, thread i owns columns 4i..4i+3
+// (D / 4 threads), and every load it needs (bias, position embedding and the
+// up to kEmbedC weight rows, clamped to the branch's channel count against
+// zero-padded token values) is issued before the sums: one round trip where
+// the loop over a run-time channel count waited on each batch of weights.
+constexpr int kEmbedC = 16;
+__global__ __launch_bounds__(512) void embed_v4_kernel(EmbedArgs a) {
+  const int row = blockIdx.x;  // b*T + t
+  const int b = row / a.T, t = row % a.T;
+  __shared__ float tok[kEmbedC];
+  const float* w;
+  const float* bias;
+  const float* src;
+  int c;
+  const int traj = a.Nv * a.Cv + a.Na * a.A;
+  if (t < a.Nv) {
+    c = a.Cv, w = a.wv, bias = a.bv, src = a.x + (size_t)b * traj + (size_t)t * a.Cv;
+  } else if (t < a.Nv + a.Na) {
+    c = a.A, w = a.wa, bias = a.ba, src = a.x + (size_t)b * traj + (size_t)a.Nv * a.Cv + (size_t)(t - a.Nv) * a.A;
+  } else {
+    c = a.Co, w = a.wo, bias = a.bo, src = a.cond + ((size_t)b * a.No + (t - a.Nv - a.Na)) * a.Co;
+  }
+  if (threadIdx.x < kEmbedC) tok[threadIdx.x] = threadIdx.x < c ? src[threadIdx.x] : 0.f;
+  const int col = threadIdx.x * 4;
+  const bool live = col < a.D;
+  const int cc = live ? col : 0;
+  const f32x4 b4 = *reinterpret_cast<const f32x4*>(bias + cc);
+  const f32x4 p4 = *reinterpret_cast<const f32x4*>(a.pe + (size_t)t * a.D + cc);
+  f32x4 w4[kEmbedC];
+#pragma unroll
+  for (int j = 0; j < kEmbedC; ++j) w4[j] = *reinterpret_cast<const f32x4*>(w + (size_t)min(j, c - 1) * a.D + cc);
+  __syncthreads();
+  f32x4 acc = b4;
+#pragma unroll
+  for (int j = 0; j < kEmbedC; ++j) acc += tok[j] * w4[j];
+  if (live) *reinterpret_cast<f32x4*>(a.h + (size_t)row * a.D + col) = acc + p4;
+}
+
 // ------------------------------------------------------------- LN + modulation
 // One wave per row; lane holds elements lane + 64 i.
 template <typename TOut>
@@ -796,7 +834,14 @@ hipError_t launch_gemv(const float* x, const void* W, bool w_bf16, const float* 
 
 hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
   if (a.Cv > 64 || a.A > 64 || a.Co > 64) return hipErrorInvalidValue;
-  launch_k(embed_kernel, a.B * a.T, 256, 0, s, a);
+  // every branch present has at least one channel (the clamp reads row c-1)
+  const bool chans = (a.Nv == 0 || a.Cv >= 1) && (a.Na == 0 || a.A >= 1) && (a.No == 0 || a.Co >= 1);
+  if (a.D % 4 == 0 && a.D <= 2048 && a.Cv <= kEmbedC && a.A <= kEmbedC && a.Co <= kEmbedC && chans) {
+    const int threads = (a.D / 4 + kWave - 1) / kWave * kWave;
+    launch_k(embed_v4_kernel, a.B * a.T, threads, 0, s, a);
+  } else {
+    launch_k(embed_kernel, a.B * a.T, 256, 0, s, a);
+  }
   return hipGetLastError();
 }
 
