@@ -316,6 +316,60 @@ def test_small_replay_replans_match_oracle(dev):
     assert paths == [L.WAM_PATH_FIRST, L.WAM_PATH_ACCEPT, L.WAM_PATH_ACCEPT]
 
 
+def test_replay_100_control_steps(dev):
+    """The closed-loop replay over 100 control steps (the replay workload's
+    length): every chunk finite, the rebinding pattern the thresholds imply
+    (first replan native; afterwards kappa_max accepted rebindings, then one
+    forced refresh, repeating), and the 100th replan, teacher-forced from the
+    device's retained state after 99, within 2e-2 of the oracle."""
+    from paper_2609_34608_amd import _lib as L
+    spec, W, m = model_for("replay", dev)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    rr_g, rr_o = rr_of(spec, L.WAM_RR_AUTO)
+    ra = _replan_args(spec)
+    rho = spec.ar_rho
+    delta = 1.0 / np.sqrt(1 - rho * rho)
+    n_ctrl = 100
+    obs = make_observations(spec, n_ctrl)
+    obs_d = torch.from_numpy(obs).to(dev)
+    pred = [obs[0]] + [(rho * obs[t - 1]).astype(np.float32) for t in range(1, n_ctrl)]
+    pred_d = torch.from_numpy(np.stack(pred)).to(dev)
+    noise_first = to_dev(make_initial_noise(spec), dev)
+    m.reset_all()
+    x_out = m.new_traj()
+    paths = []
+    for t in range(n_ctrl):
+        if t == n_ctrl - 1:
+            xb, xr, kappa = m.get_replan_state()
+        info = m.replan(obs_d[t], x_out, to_dev(make_remap_noise(spec, t), dev), cond_pred=pred_d[t],
+                        u_hat=[pred_d[t]], u=[obs_d[t]], delta=[delta], weight=[1.0], noise_first=noise_first,
+                        rr=rr_g, **ra)
+        paths.append(info.path)
+        assert torch.isfinite(x_out).all(), t
+    # with always-passing rebinding scores, kappa_max accepts then one forced refresh
+    period = [L.WAM_PATH_ACCEPT] * spec.or_kappa_max + [L.WAM_PATH_FORCED]
+    expect = [L.WAM_PATH_FIRST] + [period[(t - 1) % len(period)] for t in range(1, n_ctrl)]
+    if paths != expect:  # a rejected score restarts the cycle: check the rules instead
+        kap = 0
+        for t, pth in enumerate(paths[1:], 1):
+            assert pth in (L.WAM_PATH_ACCEPT, L.WAM_PATH_REJECT, L.WAM_PATH_FORCED), (t, pth)
+            assert (pth == L.WAM_PATH_FORCED) == (kap >= spec.or_kappa_max), (t, pth, kap)
+            kap = kap + 1 if pth == L.WAM_PATH_ACCEPT else 0
+    # the last replan against the oracle from the same retained state
+    rt = OM.ReplanRuntime(W, spec, sig, rr_o, OM.RuntimeProfile(**ra))
+    rt.set_state(xb.cpu().numpy(), xr.cpu().numpy(), kappa)
+    t = n_ctrl - 1
+    trace = deque(int(d) for d in info.decision[:info.steps] if d >= 0)
+    ref, rinfo = rt.replan(obs[t], pred[t], [pred[t]], [obs[t]], [delta], [1.0],
+                           noise_first=make_initial_noise(spec), noise_remap=make_remap_noise(spec, t),
+                           forced=trace)
+    assert info.path == rinfo.path and info.steps == rinfo.steps
+    e = rel_err(OM.action_chunk(spec, x_out.cpu().numpy()), OM.action_chunk(spec, ref))
+    print(f"replay control step {t}: path {info.path}, action chunk rel err {e:.3e}")
+    assert e <= BF16_TOL, e
+
+
 # ------------------------------------------------------------------ bf16 workloads
 def test_small_bf16_native_chunk(dev):
     spec, W, m = model_for("small", dev)
