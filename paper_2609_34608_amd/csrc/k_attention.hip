@@ -295,6 +295,7 @@ __global__ __launch_bounds__(NW * KSPLIT * 64) void attn_bf16_kernel(AttnArgs a)
   // last stage again, into slots nobody reads, which keeps the wait counts
   // uniform).  Group kgrp works on key tile KSPLIT kp + kgrp.
   const int nkp = (nkb + KSPLIT - 1) / KSPLIT;
+  const bool live = q0 < a.T;
   const std::integral_constant<bool, false> nomask{};
   const std::integral_constant<bool, true> withmask{};
   auto step = [&](auto J, int kp, auto TAIL) __attribute__((always_inline)) {
@@ -306,6 +307,9 @@ __global__ __launch_bounds__(NW * KSPLIT * 64) void attn_bf16_kernel(AttnArgs a)
     issue(std::integral_constant<int, (j + ST - 1) % ST>{}, min(kp + ST - 1, nkp - 1));
     __builtin_amdgcn_sched_barrier(0);  // loads leave before the MFMAs, not sunk below them
     const int kb = kp * KSPLIT + kgrp;
+    // a wave whose queries all lie past T (the last query block of a head)
+    // still loads and synchronises but computes nothing
+    if (!live) return;
     if constexpr (!decltype(TAIL)::value) {
       block(J, kb * kKB, nomask, kb == 0);
     } else {
