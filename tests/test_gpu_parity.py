@@ -512,6 +512,8 @@ def test_error_returns(dev):
         m.velocity(spec.K, x, c)
     with pytest.raises(WamError, match="strictly"):
         m.set_schedule(np.array([1.0, 0.5, 0.5, 0.0]))
+    with pytest.raises(WamError, match="unknown attention kernel"):
+        m.set_option(L.WAM_OPT_ATTENTION, L.WAM_ATTN_PLAIN + 1)
     m.set_schedule(sig)
     v, _ = m.velocity(0, x, c)  # still usable
     assert torch.isfinite(v).all()
