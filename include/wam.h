@@ -135,7 +135,7 @@ typedef struct wam_handle *wam_t;
 
 /* Model configuration.  D % 64 == 0 (D <= 2048), D % H == 0, head size D/H in
  * {32, 64}, Cv <= 16, A <= 16, Co <= 64; bf16 mode additionally needs
- * D/H == 64, D % 128 == 0 and F % 128 == 0.  Nv >= 0, Na >= 0, Nv + Na >= 1:
+ * D/H == 64 and F % 128 == 0 (any head count, odd ones included).  Nv >= 0, Na >= 0, Nv + Na >= 1:
  * a model of an independently executed pair has only video (Na = 0) or only
  * action (Nv = 0) tokens; Cv and A stay >= 1 (their weights exist). */
 typedef struct {

@@ -41,6 +41,7 @@ constexpr TileCfg kCfgs[] = {
     {128, 128, 2, 2, 4, 64},  // 23
     {192, 256, 2, 4, 2, 64},  // 24
     {320, 256, 2, 4, 2, 64},  // 25
+    {64, 64, 4, 1, 4, 32},    // 26 (QKV outputs of 64 mod 128 columns: odd head counts)
 };
 constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
@@ -78,7 +79,8 @@ hipError_t launch_role(const GemmArgs& a, int cfg, int splits, hipStream_t s) {
     case 22: return launch_c<22, ROLE>(a, splits, s);
     case 23: return launch_c<23, ROLE>(a, splits, s);
     case 24: return launch_c<24, ROLE>(a, splits, s);
-    default: return launch_c<25, ROLE>(a, splits, s);
+    case 25: return launch_c<25, ROLE>(a, splits, s);
+    default: return launch_c<26, ROLE>(a, splits, s);
   }
 }
 
@@ -188,7 +190,9 @@ GemmPlan plan_gemm(int M, int N, int K, int epi) {
     return p;
   }
   if (epi == EPI_QKV) {
-    p.cfg = N % 128 != 0 ? 3 : K % 64 == 0 ? 19 : 1;
+    // whole heads per wave: 64 columns per wave; an odd head count leaves
+    // N = 192 H a multiple of 64 only, which takes one wave column of 64
+    p.cfg = N % 128 != 0 ? 26 : K % 64 == 0 ? 19 : 1;
     return p;
   }
   if (N >= 2048 && N % 128 == 0 && K <= 1024) {

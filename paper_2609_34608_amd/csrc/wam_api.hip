@@ -55,7 +55,7 @@ int make_dims(const wam_config* c, Dims* d, std::string* why) {
   if (dh != 32 && dh != 64) return bad("head size D/H must be 32 or 64");
   if (c->dtype == WAM_BF16) {
     if (dh != 64) return bad("bf16 mode needs head size 64");
-    if (c->D % 128 || c->F % 128) return bad("bf16 mode needs D and F multiples of 128");
+    if (c->F % 128) return bad("bf16 mode needs F a multiple of 128");
   } else {
     if (c->F % 64) return bad("F must be a multiple of 64");
   }

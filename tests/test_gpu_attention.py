@@ -166,3 +166,25 @@ def test_bf16_degenerate_shapes_match_oracle(dev, shape):
         print(f"{shape} B={B} T={spec.T} step {k} velocity rel err {e:.3e}")
         assert e <= BF16_TOL, (k, e)
     m.close()
+
+
+@pytest.mark.parametrize("D,H", [(192, 3), (1088, 17)])
+def test_bf16_odd_head_counts_match_oracle(dev, D, H):
+    """bf16 mode with an odd number of heads: the QKV output width 192 H is a
+    multiple of 64 but not of 128 (its own GEMM tile); D not a multiple of 256
+    takes the generic LayerNorm, and D = 1088 the row-wise final layer."""
+    from paper_2609_34608_amd import runtime as R
+    spec = get_workload("small").replace(L=1, D=D, H=H, F=4 * D, Nv=40, Na=16, No=8, B=2)
+    W = make_weights(spec, bias_std=0.02, gain_std=0.1)
+    m = R.WamModel(R.config_of(spec), W, device=dev)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    for k in (0, 5):
+        v, _ = m.velocity(k, to_dev(x0, dev), to_dev(cond, dev))
+        ref = OD.velocity(W, spec, x0, cond, sig[k])
+        e = rel_err(v.cpu().numpy(), ref)
+        print(f"D={D} H={H} step {k} velocity rel err {e:.3e}")
+        assert e <= BF16_TOL, (k, e)
+    m.close()
