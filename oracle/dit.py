@@ -44,7 +44,7 @@ def silu(x):
 def gelu_tanh(x):
     """GELU, tanh approximation: x/2 * (1 + tanh(sqrt(2/pi) (x + 0.044715 x^3)))."""
     x = as64(x)
-    return 0.5 * x * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (x + 0.044715 * x ** 3)))
+    return 0.5 * x * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (x + 0.044715 * (x * x * x))))
 
 
 def layer_norm(x, eps):
@@ -133,11 +133,37 @@ def embed_tokens(W, spec, x, cond):
 # --------------------------------------------------------------------------
 # transformer layer
 # --------------------------------------------------------------------------
+# Worker threads for the loop over (sample, head) pairs in `attention`.  The
+# pairs are independent problems, so the result is the same for any count;
+# long oracle runs (the full-size chunk fixtures) raise it to the core count.
+ATTENTION_THREADS = 1
+
+
 def attention(q, k, v):
-    """Bidirectional softmax attention over all rows, q/k/v [..., T, dh]."""
+    """Bidirectional softmax attention over all rows, q/k/v [..., T, dh].
+
+    Each (sample, head) pair is an independent attention problem, so they are
+    taken one at a time: the T x T score matrix of a single head is the
+    largest array held (about 0.8 GB in float64 at T = 10176), where all heads
+    at once would need tens of GB.  The result does not depend on this loop.
+    """
     q, k, v = as64(q), as64(k), as64(v)
-    s = q @ np.swapaxes(k, -1, -2) / np.sqrt(q.shape[-1])
-    return softmax(s, axis=-1) @ v
+    out = np.empty(q.shape[:-1] + (v.shape[-1],), f64)
+    scale = 1.0 / np.sqrt(q.shape[-1])
+
+    def one(idx):
+        s = (q[idx] @ k[idx].T) * scale
+        out[idx] = softmax(s, axis=-1) @ v[idx]
+
+    pairs = list(np.ndindex(*q.shape[:-2]))
+    if ATTENTION_THREADS > 1 and len(pairs) > 1:
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(ATTENTION_THREADS) as ex:
+            list(ex.map(one, pairs))
+    else:
+        for idx in pairs:
+            one(idx)
+    return out
 
 
 def qkv_heads(W, spec, l, u):
