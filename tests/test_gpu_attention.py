@@ -15,7 +15,7 @@ import pytest
 
 from oracle import dit as OD
 from synth import get_workload, make_weights, make_initial_noise, make_observations
-from gpu_common import device, to_dev, rel_err, f32_sigmas
+from gpu_common import device, to_dev, rel_err, f32_sigmas, layer_update_errors, BF16_UPDATE_TOL
 
 pytestmark = pytest.mark.gpu
 
@@ -51,6 +51,9 @@ def test_bf16_attention_lengths_match_oracle(dev, lengths, variant):
     x0 = make_initial_noise(spec)
     cond = make_observations(spec, 0)[0]
     for k in (0, 6):
+        for l, e in layer_update_errors(m, W, spec, k, x0, cond, sig[k], [0, 1], dev):
+            print(f"T={spec.T} {variant} step {k} layer {l} update rel err {e:.3e}")
+            assert e <= BF16_UPDATE_TOL, (spec.T, k, l, e)
         v, _ = m.velocity(k, to_dev(x0, dev), to_dev(cond, dev))
         ref = OD.velocity(W, spec, x0, cond, sig[k])
         e = rel_err(v.cpu().numpy(), ref)
@@ -160,6 +163,9 @@ def test_bf16_degenerate_shapes_match_oracle(dev, shape):
     x0 = make_initial_noise(spec)
     cond = make_observations(spec, 0)[0]
     for k in (0, 5):
+        for l, e in layer_update_errors(m, W, spec, k, x0, cond, sig[k], [0, 1], dev):
+            print(f"{shape} B={B} T={spec.T} step {k} layer {l} update rel err {e:.3e}")
+            assert e <= BF16_UPDATE_TOL, (k, l, e)
         v, _ = m.velocity(k, to_dev(x0, dev), to_dev(cond, dev))
         ref = OD.velocity(W, spec, x0, cond, sig[k])
         e = rel_err(v.cpu().numpy(), ref)
@@ -182,6 +188,9 @@ def test_bf16_odd_head_counts_match_oracle(dev, D, H):
     x0 = make_initial_noise(spec)
     cond = make_observations(spec, 0)[0]
     for k in (0, 5):
+        for l, e in layer_update_errors(m, W, spec, k, x0, cond, sig[k], [0], dev):
+            print(f"D={D} H={H} step {k} layer {l} update rel err {e:.3e}")
+            assert e <= BF16_UPDATE_TOL, (k, l, e)
         v, _ = m.velocity(k, to_dev(x0, dev), to_dev(cond, dev))
         ref = OD.velocity(W, spec, x0, cond, sig[k])
         e = rel_err(v.cpu().numpy(), ref)

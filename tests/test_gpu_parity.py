@@ -13,7 +13,8 @@ import torch
 
 from oracle import dit as OD, method as OM
 from synth import get_workload, make_weights, make_initial_noise, make_observations, make_remap_noise
-from gpu_common import device, to_dev, rel_err, rr_of, f32_sigmas, model_for
+from gpu_common import (device, to_dev, rel_err, rr_of, f32_sigmas, model_for, layer_update_errors,
+                        BF16_UPDATE_TOL)
 
 pytestmark = pytest.mark.gpu
 
@@ -388,6 +389,24 @@ def test_small_bf16_native_chunk(dev):
     ea = rel_err(OM.action_chunk(spec, x.cpu().numpy()), OM.action_chunk(spec, ref))
     print(f"small bf16 action chunk rel err {ea:.3e}")
     assert ea <= BF16_TOL
+
+
+@pytest.mark.parametrize("k", [0, 7])
+def test_small_bf16_layer_updates_every_layer(dev, k):
+    """Every layer of the small model (the replay workload's kernels: the
+    M = 864 GEMM tiles, the key-split attention) checked on its own: the
+    device's update of each layer against the oracle's on the same input,
+    every row.  Removing attention or the MLP moves this quantity by at least
+    ten times the tolerance (tests/test_oracle_sensitivity.py)."""
+    spec, W, m = model_for("small", dev)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    errs = layer_update_errors(m, W, spec, k, x0, cond, sig[k], list(range(spec.L)), dev)
+    print(f"small bf16 step {k} layer-update rel err: " + " ".join(f"{e:.2e}" for _, e in errs))
+    for l, e in errs:
+        assert e <= BF16_UPDATE_TOL, (l, e)
 
 
 @pytest.mark.parametrize("name,layers", [("mid", (0, 11)), ("large", (0, 17))])
