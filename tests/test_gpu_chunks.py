@@ -35,6 +35,8 @@ def dev():
 @pytest.mark.parametrize("name", ["mid", "large"])
 def test_native_chunk_matches_oracle_fixture(dev, name):
     path = os.path.join(GOLDEN, f"native_chunk_{name}.npz")
+    if not os.path.exists(path):
+        pytest.skip(f"fixture {os.path.basename(path)} not written yet (tests/golden/make_chunk_goldens.py)")
     fx = np.load(path)
     spec, W, m = model_for(name, dev)
     sig = f32_sigmas(spec.K)
