@@ -1,13 +1,21 @@
 """Benchmark: WAMachine-style replans on one MI355X.
 
-A timed step is one closed-loop replan of the small joint video/action DiT
-(12 layers, hidden 768, 12 heads, MLP 3072; 768 video + 32 action + 64
-observation tokens; 10 flow steps; bf16 contractions): Trajectory Remapping of
-the previous replan's state, an anticipatory prefix of 2 steps under the
-predicted observation, the consistency score and rebinding (or restart), and
-Residual Rescaling inside every denoising step, all through libwam.  Inputs
-(weights, noise, AR(1) observations) are seeded, synthetic and resident in HBM
-before timing starts.
+A timed step is one closed-loop replan of the large joint video/action DiT
+(28 layers, hidden 1536, 24 heads, MLP 6144; 8 frames of 30x40 = 9600 video +
+64 action (14-dim) + 512 observation tokens; 20 flow steps; bf16
+contractions): Trajectory Remapping of the previous replan's state (entry at
+stage 10), an anticipatory prefix of 4 steps under the predicted observation,
+the consistency score and rebinding (or restart), and Residual Rescaling
+inside every denoising step, all through libwam.  Inputs (weights, noise,
+AR(1) observations) are seeded, synthetic and resident in HBM before timing
+starts.  `value` counts denoising steps per second.
+
+The same line carries: the native full re-denoise of that model, the
+dominant kernel against the bf16 MFMA peak (roofline), the adaptation
+kernels against HBM, the achievable-peak probes, the float64 oracle on the
+host (cpu_baseline), and the closed-loop replay of the small model (12
+layers, hidden 768, T = 864, 10 steps) as extra keys.  --workload selects
+another model for the headline.
 
 Prints one JSON line.  --gpus N > 1 is refused: the library runs on one GPU.
 """
@@ -117,12 +125,16 @@ def lookup_traffic(workload: str, cls: str):
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=30)
-    p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", default="replay",
-                   help="replay (small model) | mid | large | idm (independent video / action pair)")
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--workload", default="large",
+                   help="large (default: the 16-frame model) | mid | replay (small model) | idm (independent "
+                        "video / action pair)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-native", action="store_true")
+    p.add_argument("--no-probes", action="store_true", help="skip the achievable-peak probes")
+    p.add_argument("--no-replay", action="store_true",
+                   help="skip the extra small-model closed-loop replay figures")
     p.add_argument("--cpu-sample-steps", type=int, default=5)
     p.add_argument("--rr-mode", default="auto", choices=["auto", "force_skip", "force_full", "off"],
                    help="residual-rescaling mode of the timed replans")
@@ -173,6 +185,45 @@ def main():
     if args.workload in PAIRS:
         idm_main(args)
         return
+    out = measure(args, args.workload, args.steps, args.warmup, cpu=not args.no_cpu_baseline,
+                  native=not args.no_native, adapt=True, copy_probe_mib=args.copy_probe_mib)
+    if not args.no_probes:
+        out["achievable"] = achievable_peaks()
+        ach = out["achievable"]["mfma_bf16_16x16x32_tflops"]
+        out["roofline"]["frac_of_achievable"] = round(out["roofline"]["achieved"] / ach, 5)
+        out["mfma_frac_dit_of_achievable"] = round(out["dit_tflops"] / ach, 5)
+        cg = out["achievable"]["copy_gbs"]
+        for v in out.get("adaptation_kernels", {}).values():
+            v["frac_of_achievable_copy"] = round(v["GB/s"] / cg, 4)
+    if not args.no_replay and args.workload != "replay":
+        r = measure(args, "replay", 30, 5, cpu=False, native=not args.no_native, adapt=False)
+        out["replay"] = {k: r[k] for k in ("value", "unit", "ms_per_step", "action_chunks_per_s",
+                                           "denoise_steps_per_replan", "dit_tflops", "mfma_frac_dit",
+                                           "native_chunk_ms", "reuse_latency_speedup", "reuse_stats")
+                         if k in r}
+        out["replay"]["workload"] = r["config"]["workload"]
+        out["replay"]["dominant_kernel"] = {k: r["roofline"][k]
+                                            for k in ("kernel", "achieved", "frac", "avg_launch_us")}
+    print(json.dumps(out), flush=True)
+
+
+def achievable_peaks():
+    """What the chip reaches in practice: the bf16 MFMA issue rate on register
+    operands (both MFMA shapes) and a streaming copy of 1 GiB."""
+    from paper_2609_34608_amd import runtime as R
+    t16, _ = R.probe_mfma_bf16(shape=0)
+    t32, _ = R.probe_mfma_bf16(shape=1)
+    gbs, _ = R.probe_copy(1 << 30, reps=5)
+    return {"mfma_bf16_16x16x32_tflops": round(t16, 1), "mfma_bf16_32x32x16_tflops": round(t32, 1),
+            "copy_gbs": round(gbs, 1),
+            "method": "wam_probe_mfma_bf16 (1024 blocks x 4 waves, 20000 rounds of independent MFMA chains "
+                      "on register operands) and wam_probe_copy (1 GiB device copy, 16-byte accesses, read + "
+                      "write bytes counted), HIP events"}
+
+
+def measure(args, name, steps, warmup, cpu, native, adapt, copy_probe_mib=0):
+    """Closed-loop replans of workload `name` (one timed step = one replan);
+    returns the bench record."""
     import numpy as np
     import torch
 
@@ -180,7 +231,7 @@ def main():
     from paper_2609_34608_amd import runtime as R
     from synth import get_workload, make_weights, make_initial_noise, make_observations, make_remap_noise
 
-    spec = get_workload(args.workload)
+    spec = get_workload(name)
     dev = torch.device("cuda:0")
     W = make_weights(spec)
     m = R.WamModel(R.config_of(spec), W, device=dev, own_stream=args.exec == "graph")
@@ -198,7 +249,7 @@ def main():
              "off": L.WAM_RR_OFF}
     rr = R.rr_profile(q, s_, e, modes[args.rr_mode], spec.rr_alpha_min, spec.rr_alpha_max, spec.rr_eps,
                       spec.rr_gamma_cos, spec.rr_gamma_fit)
-    n_ctrl = 1 + args.warmup + args.steps
+    n_ctrl = 1 + warmup + steps
     obs = make_observations(spec, n_ctrl)
     rho = spec.ar_rho
     delta = 1.0 / np.sqrt(1.0 - rho * rho)
@@ -216,8 +267,8 @@ def main():
         return m.replan(cr, x_out, remap_noise[t], cond_pred=cp, u_hat=[cp], u=[cr], delta=[delta],
                         weight=[1.0], noise_first=noise_first, rr=rr, **ra)
 
-    if args.copy_probe_mib:
-        n = args.copy_probe_mib * 2 ** 18
+    if copy_probe_mib:
+        n = copy_probe_mib * 2 ** 18
         src = torch.ones(n, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
@@ -228,7 +279,7 @@ def main():
     t = 0
     replan(t)  # first replan: native K steps from noise
     t += 1
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         replan(t)
         t += 1
     # untimed attribution pass over one replan: which kernel class dominates
@@ -250,7 +301,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     infos = []
-    for _ in range(args.steps):
+    for _ in range(steps):
         infos.append(replan(t))
         t += 1
     torch.cuda.synchronize()
@@ -261,9 +312,9 @@ def main():
     n_steps = sum(i.steps for i in infos)
     layers_eval = sum(i.steps * spec.L - i.layers_skipped for i in infos)
     flops = spec.flops_per_layer() * layers_eval
-    ms_per_step = 1000.0 * elapsed / args.steps
+    ms_per_step = 1000.0 * elapsed / steps
     steps_per_s = n_steps / elapsed
-    chunks_per_s = args.steps / elapsed
+    chunks_per_s = steps / elapsed
     n_att = sum(i.rr_attempts for i in infos)
     n_reuse = sum(i.rr_reuses for i in infos)
     skip = sum(i.layers_skipped for i in infos)
@@ -277,8 +328,8 @@ def main():
         "value": round(steps_per_s, 3),
         "unit": "denoise steps/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": warmup,
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -295,13 +346,13 @@ def main():
             "attention": args.attention,
         },
         "action_chunks_per_s": round(chunks_per_s, 3),
-        "denoise_steps_per_replan": n_steps / args.steps,
+        "denoise_steps_per_replan": n_steps / steps,
         "mfma_frac_dit": round(flops / elapsed / 1e12 / MFMA_BF16_PEAK_TFLOPS, 5),
         "dit_tflops": round(flops / elapsed / 1e12, 3),
         "reuse_stats": {"rr_accept": n_reuse / n_att if n_att else None,
                         "rr_skip_frac": skip / dense if dense else None,
                         "or_accept": n_bind / n_start if n_start else None,
-                        "or_coverage": n_bind / args.steps},
+                        "or_coverage": n_bind / steps},
         "roofline": {
             "kernel": L.KERNEL_CLASS_NAMES[dom],
             "bound": "mfma",
@@ -316,8 +367,41 @@ def main():
         },
     }
 
-    # adaptation kernels at this workload's size: two extra (untimed) replans
-    # with reuse forced so that the gate, the injection and the refresh all run
+    if adapt:
+        out["adaptation_kernels"] = adaptation_kernels(m, spec, replan, t)
+
+    if native:
+        # full re-denoise of the same model: K native steps from noise per chunk
+        xn = m.new_traj()
+        nrep = max(3, steps // 5)
+        m.reset_all()
+        xn.copy_(noise_first)
+        m.continue_(0, K, xn, obs_d[0])
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(nrep):
+            xn.copy_(noise_first)
+            m.continue_(0, K, xn, obs_d[i + 1])
+        torch.cuda.synchronize()
+        nat = (time.perf_counter() - t0) / nrep
+        out["native_chunk_ms"] = round(1000.0 * nat, 4)
+        out["native_steps_per_s"] = round(K / nat, 3)
+        out["reuse_latency_speedup"] = round(nat / (elapsed / steps), 4)
+
+    if cpu:
+        out["cpu_baseline"] = (cpu_baseline_layer(spec, W) if spec.name == "large"
+                               else cpu_baseline(spec, W, obs, args.cpu_sample_steps))
+    m.close()
+    return out
+
+
+def adaptation_kernels(m, spec, replan, t):
+    """Residual-Rescaling kernels at the workload's size: two extra (untimed)
+    replans with reuse forced, so that the gate, the injection and the refresh
+    all run, each launch timed by its dispatch stamps."""
+    from paper_2609_34608_amd import _lib as L
+    from paper_2609_34608_amd import runtime as R
+    q, s_, e = spec.rr_bounds
     rr_force = R.rr_profile(q, s_, e, L.WAM_RR_FORCE_SKIP, spec.rr_alpha_min, spec.rr_alpha_max, spec.rr_eps,
                             spec.rr_gamma_cos, spec.rr_gamma_fit)
     ad = [L.WAM_KC_RR_GATE, L.WAM_KC_RR_INJECT, L.WAM_KC_RR_REFRESH]
@@ -334,30 +418,7 @@ def main():
             adapt[L.KERNEL_CLASS_NAMES[kc]] = {"launches": n_, "avg_us": round(1000.0 * ms_ / n_, 3),
                                                "bytes_per_launch": bytes_ / n_, "GB/s": round(gbs, 1),
                                                "frac_hbm": round(gbs / HBM_PEAK_GBS, 4)}
-    out["adaptation_kernels"] = adapt
-
-    if not args.no_native:
-        # full re-denoise of the same model: K native steps from noise per chunk
-        xn = m.new_traj()
-        nrep = max(3, args.steps // 5)
-        m.reset_all()
-        xn.copy_(noise_first)
-        m.continue_(0, K, xn, obs_d[0])
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for i in range(nrep):
-            xn.copy_(noise_first)
-            m.continue_(0, K, xn, obs_d[i + 1])
-        torch.cuda.synchronize()
-        nat = (time.perf_counter() - t0) / nrep
-        out["native_chunk_ms"] = round(1000.0 * nat, 4)
-        out["native_steps_per_s"] = round(K / nat, 3)
-        out["reuse_latency_speedup"] = round(nat / (elapsed / args.steps), 4)
-
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(spec, W, obs, args.cpu_sample_steps)
-    print(json.dumps(out), flush=True)
-    m.close()
+    return adapt
 
 
 def idm_main(args):
@@ -739,17 +800,35 @@ def diagnostics(args):
     print(json.dumps(out), flush=True)
 
 
+def host_info():
+    """Host cores, CPU model and BLAS threads of the machine the oracle runs on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        from threadpoolctl import threadpool_info
+        blas = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:
+        blas = None
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        affinity = None
+    return {"host_cpus": os.cpu_count(), "affinity_cpus": affinity, "cpu_model": model, "blas_threads": blas}
+
+
 def cpu_baseline(spec, W, obs, n_steps, single=False):
     """The float64 oracle on the host: a bounded sample of Euler steps of the
     same model (the continuation of one accepted replan), timed."""
-    import numpy as np
     from oracle import method as OM
     from synth import make_initial_noise
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
-    except Exception:
-        threads = os.cpu_count() or 1
+    info = host_info()
     sig = OM.flow_schedule(spec.K)
     q, s, e = spec.rr_bounds
     rr = OM.RRProfile(q, s, e, spec.rr_alpha_min, spec.rr_alpha_max, spec.rr_eps, spec.rr_gamma_cos,
@@ -759,10 +838,36 @@ def cpu_baseline(spec, W, obs, n_steps, single=False):
     t0 = time.perf_counter()
     OM.denoise(W, spec, x, obs[0], sig, k0, spec.K, rr, OM.LayerState())
     dt = time.perf_counter() - t0
-    return {"value": round(n_steps / dt, 5), "unit": "denoise steps/s", "cores": int(threads),
+    return {"value": round(n_steps / dt, 5), "unit": "denoise steps/s", "cores": info["blas_threads"],
             "kind": "oracle",
             "sample": f"{n_steps} float64 Euler steps with residual rescaling of the same model "
-                      f"(steps {k0}..{spec.K - 1}), {dt:.1f} s"}
+                      f"(steps {k0}..{spec.K - 1}), {dt:.1f} s", **info}
+
+
+def cpu_baseline_layer(spec, W):
+    """The float64 oracle on the host at the large workload: one DiT layer of
+    the model (full sequence, every head, the oracle's serial head loop),
+    timed, and scaled to one denoising step of L layers.  The embedding and
+    the output heads of a step are under 1% of its work and are left out."""
+    import numpy as np
+    from oracle import dit as OD
+    from synth import make_initial_noise, make_observations
+    info = host_info()
+    x = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    c = OD.cond_vector(W, 1.0)
+    h = OD.embed_tokens(W, spec, x, cond)
+    t0 = time.perf_counter()
+    h1 = OD.dit_layer(W, spec, 0, h, c)
+    dt = time.perf_counter() - t0
+    assert np.isfinite(h1).all()
+    step_s = dt * spec.L
+    return {"value": round(1.0 / step_s, 6), "unit": "denoise steps/s", "cores": info["blas_threads"],
+            "kind": "oracle",
+            "sample": f"one float64 DiT layer of the {spec.name} model (T={spec.T}, {spec.H} heads), "
+                      f"{dt:.1f} s, x {spec.L} layers = {step_s:.0f} s per denoising step; the oracle's "
+                      f"matrix products use {info['blas_threads']} BLAS threads, its elementwise work one",
+            **info}
 
 
 if __name__ == "__main__":

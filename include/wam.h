@@ -347,6 +347,30 @@ int wam_profile_enable(wam_t h, int kc, int enable, int max_launches);
  * Synchronises. */
 int wam_profile_read(wam_t h, int kc, double *total_ms, int64_t *launches, double *work);
 
+/* Achievable-peak probes (no handle; synchronous on hip_stream, which may be
+ * NULL for the default stream).  They measure what the chip reaches in
+ * practice, beside the vendor peaks that the roofline fractions use.
+ *
+ * wam_probe_mfma_bf16: n_blocks blocks of 256 threads each run iters rounds
+ * of independent bf16 MFMA chains on register operands (shape 0:
+ * v_mfma_f32_16x16x32_bf16, the instruction of the GEMM and attention
+ * kernels; shape 1: v_mfma_f32_32x32x16_bf16), 131072 FLOP per wave per
+ * round, after one untimed warm-up launch.  sink: device float[n_blocks *
+ * 256], caller-owned, receives one value per thread.  Outputs the rate in
+ * TFLOP/s and the timed launch in ms.
+ *
+ * wam_probe_copy: copies bytes (a multiple of 16, both pointers 16-byte
+ * aligned, device, caller-owned, not overlapping) from src to dst reps times
+ * after one warm-up; outputs the rate counting the bytes read plus written
+ * (GB/s, 1e9) and the time per copy in ms.
+ *
+ * Both return WAM_E_ARG for invalid arguments and WAM_E_HIP for a runtime
+ * error (no handle, so no message). */
+int wam_probe_mfma_bf16(void *hip_stream, int shape, int n_blocks, int iters, float *sink, double *tflops,
+                        double *ms);
+int wam_probe_copy(void *hip_stream, const void *src, void *dst, size_t bytes, int reps, double *gbs,
+                   double *ms);
+
 #ifdef __cplusplus
 }
 #endif

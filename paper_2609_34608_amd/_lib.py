@@ -109,6 +109,10 @@ EXPORTS = {
     "wam_profile_enable": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int]),
     "wam_profile_read": (C.c_int, [C.c_void_p, C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int64),
                                    C.POINTER(C.c_double)]),
+    "wam_probe_mfma_bf16": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.POINTER(C.c_double),
+                                      C.POINTER(C.c_double)]),
+    "wam_probe_copy": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_int, C.POINTER(C.c_double),
+                                 C.POINTER(C.c_double)]),
 }
 
 

@@ -35,7 +35,7 @@ COMMON = [
     "-Wno-unused-result", f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 
-SOURCES = ["k_small.hip", "k_gemm.hip", "k_attention.hip", "wam_api.hip"]
+SOURCES = ["k_small.hip", "k_gemm.hip", "k_attention.hip", "k_probe.hip", "wam_api.hip"]
 
 
 def _compile(src: str) -> str:

@@ -325,3 +325,30 @@ class IdmPair:
                                    self.cond_action)
         ia = self.action.replan(self.cond_action, x_action, noise_remap_action, **(action_kw or {}))
         return iv, ia
+
+
+def probe_mfma_bf16(shape: int = 0, n_blocks: int = 1024, iters: int = 20000, device="cuda:0"):
+    """Achievable bf16 MFMA rate (wam_probe_mfma_bf16): returns (TFLOP/s, ms)."""
+    lib = abi.lib()
+    sink = torch.empty(n_blocks * 256, dtype=torch.float32, device=device)
+    stream = C.c_void_p(torch.cuda.current_stream(sink.device).cuda_stream)
+    tf, ms = C.c_double(), C.c_double()
+    rc = lib.wam_probe_mfma_bf16(stream, shape, n_blocks, iters, _ptr(sink), C.byref(tf), C.byref(ms))
+    if rc != abi.WAM_OK:
+        raise WamError(f"wam_probe_mfma_bf16: {lib.wam_status_string(rc).decode()}")
+    return tf.value, ms.value
+
+
+def probe_copy(nbytes: int = 1 << 30, reps: int = 5, device="cuda:0"):
+    """Achievable streaming copy rate (wam_probe_copy): returns (GB/s counting
+    read + write bytes, ms per copy)."""
+    lib = abi.lib()
+    n = nbytes // 4
+    src = torch.ones(n, dtype=torch.float32, device=device)
+    dst = torch.empty_like(src)
+    stream = C.c_void_p(torch.cuda.current_stream(src.device).cuda_stream)
+    gbs, ms = C.c_double(), C.c_double()
+    rc = lib.wam_probe_copy(stream, _ptr(src), _ptr(dst), n * 4, reps, C.byref(gbs), C.byref(ms))
+    if rc != abi.WAM_OK:
+        raise WamError(f"wam_probe_copy: {lib.wam_status_string(rc).decode()}")
+    return gbs.value, ms.value

@@ -29,10 +29,13 @@ TIME_EMB_DIM = 256  # sinusoidal timestep features fed to the conditioning MLP
 def bf16_round(a: np.ndarray) -> np.ndarray:
     """Round float32 values to the nearest bfloat16 (ties to even), as float32."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    u = (u + 0x7FFF + lsb) & 0xFFFF0000
-    return u.astype(np.uint32).view(np.float32).reshape(a.shape)
+    u = a.view(np.uint32)
+    # add half an ulp of bf16 minus one, plus the lsb that is kept (ties to
+    # even), then truncate; 32-bit wrap-around only ever reaches bits that
+    # the mask drops
+    r = u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
+    r &= np.uint32(0xFFFF0000)
+    return r.view(np.float32).reshape(a.shape)
 
 
 def weight_manifest(w: WorkloadSpec) -> list[tuple[str, tuple[int, ...], str]]:
