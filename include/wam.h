@@ -78,6 +78,7 @@ extern "C" {
 #define WAM_ADAPT_RESET_LAYER 2 /* args: NULL; drop retained (p_a, R_a)      */
 #define WAM_ADAPT_RESET_ALL 3   /* args: NULL; drop layer and replan state   */
 #define WAM_ADAPT_SET_REPLAN 4  /* args: const wam_replan_state_args*        */
+#define WAM_ADAPT_REBIND 5      /* args: const wam_rebind_args*              */
 
 /* ---- replan paths (Sec. 3.4) ------------------------------------------- */
 #define WAM_PATH_FIRST 0  /* first replan: K steps from fresh noise           */
@@ -196,6 +197,23 @@ typedef struct {
   const float *noise; /* device [B][traj] N(0,1); unmapped slots get sigma_b0*noise */
   float *x_out;       /* device [B][traj]: remapped initialisation              */
 } wam_remap_args;
+
+/* Observation Rebinding's rebinding step (Sec. 3.2): the retained denoising
+ * state (the working latent an anticipatory prefix produced under the
+ * predicted condition c_hat, the latent captured at stage r, and the Residual
+ * Rescaling layer state, which persists across the rebinding point, Sec. 3.3)
+ * continues under the real condition c.  The library copies cond into its own
+ * condition buffer (stream-ordered; the caller's buffer may be reused once the
+ * stream passes this point) and from then on a NULL cond in wam_velocity,
+ * wam_denoise_step, wam_continue and wam_hidden means that bound condition.
+ * Nothing else of the retained state changes; the rebinding counter kappa
+ * and the decision S < tau and kappa < kappa_max belong to wam_replan, which
+ * performs the same step on its accept path (and leaves its real condition
+ * bound after every replan).  cond: device [B][No][Co], may be NULL only when
+ * No == 0.  WAM_E_ARG for a NULL cond otherwise. */
+typedef struct {
+  const float *cond;
+} wam_rebind_args;
 
 /* Adopt an externally held replan state (teacher forcing / resume). */
 typedef struct {
@@ -331,6 +349,11 @@ int wam_replan(wam_t h, const wam_replan_args *args, wam_replan_info *info);
  * without a begin runs the whole replan.  A second begin before end is
  * WAM_E_STATE. */
 int wam_replan_begin(wam_t h, const wam_replan_args *args);
+/* While a replan is open (after wam_replan_begin, before wam_replan_end) the
+ * other calls that touch the handle's state (wam_velocity, wam_denoise_step,
+ * wam_continue, wam_hidden, wam_adapt_state except RESET_ALL,
+ * wam_consistency_score, wam_get_replan_state, wam_set_schedule,
+ * wam_set_option) return WAM_E_STATE; RESET_ALL abandons the open replan. */
 int wam_replan_end(wam_t h, const wam_replan_args *args, wam_replan_info *info);
 /* Copies of the retained replan state (device [B][traj] each; may be NULL). */
 int wam_get_replan_state(wam_t h, float *x_bar, float *x_r, int32_t *kappa);

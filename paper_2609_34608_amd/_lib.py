@@ -16,7 +16,7 @@ WAM_OK, WAM_E_ARG, WAM_E_SHAPE, WAM_E_STATE, WAM_E_HIP, WAM_E_WORKSPACE, WAM_E_U
 WAM_FP32, WAM_BF16 = 0, 1
 WAM_RR_OFF, WAM_RR_AUTO, WAM_RR_FORCE_SKIP, WAM_RR_FORCE_FULL = 0, 1, 2, 3
 WAM_RR_JOINT, WAM_RR_SINGLE = 0, 1
-WAM_ADAPT_REMAP, WAM_ADAPT_RESET_LAYER, WAM_ADAPT_RESET_ALL, WAM_ADAPT_SET_REPLAN = 1, 2, 3, 4
+WAM_ADAPT_REMAP, WAM_ADAPT_RESET_LAYER, WAM_ADAPT_RESET_ALL, WAM_ADAPT_SET_REPLAN, WAM_ADAPT_REBIND = 1, 2, 3, 4, 5
 WAM_PATH_FIRST, WAM_PATH_ACCEPT, WAM_PATH_REJECT, WAM_PATH_FORCED, WAM_PATH_DIRECT = 0, 1, 2, 3, 4
 WAM_MAX_BATCH, WAM_MAX_COMPONENTS, WAM_MAX_STEPS = 16, 8, 64
 WAM_OPT_DEVICE_DECISION, WAM_OPT_GRAPHS, WAM_OPT_ATTENTION = 1, 2, 3
@@ -50,6 +50,10 @@ class WamRemapArgs(C.Structure):
     _fields_ = [("x_bar", C.c_void_p), ("x_r", C.c_void_p), ("sigma_r", C.c_float), ("sigma_b0", C.c_float),
                 ("shift_action", C.c_int32), ("shift_video", C.c_int32), ("noise", C.c_void_p),
                 ("x_out", C.c_void_p)]
+
+
+class WamRebindArgs(C.Structure):
+    _fields_ = [("cond", C.c_void_p)]
 
 
 class WamReplanStateArgs(C.Structure):

@@ -744,21 +744,40 @@ __global__ __launch_bounds__(256) void copy_f32x4_kernel(const f32x4* __restrict
 }
 
 // ------------------------------------------------------------- Trajectory Remapping
-// rms of (x^r - x_bar)/sigma_r per (sample, branch) over the whole branch.
-__global__ void remap_rms_kernel(RemapArgs a) {
+// rms of (x^r - x_bar)/sigma_r per (sample, branch) over the whole branch, in
+// two launches: each branch is cut into kRemapChunks equal runs, one block
+// per run sums its squares (float64), then one thread per (sample, branch)
+// adds the run sums in run order (the same bits on every call).
+__global__ __launch_bounds__(256) void remap_partial_kernel(RemapArgs a) {
   __shared__ double sh[16];
-  const int b = blockIdx.x / 2, br = blockIdx.x % 2;
+  const int sb = blockIdx.y;  // sample * 2 + branch
+  const int b = sb / 2, br = sb % 2;
   const int traj = a.Nv * a.Cv + a.Na * a.A;
   const int lo = br == 0 ? 0 : a.Nv * a.Cv;
   const int hi = br == 0 ? a.Nv * a.Cv : traj;
+  const int per = (hi - lo + kRemapChunks - 1) / kRemapChunks;
+  const int c0 = lo + (int)blockIdx.x * per;
+  const int c1 = min(c0 + per, hi);
+  const float* xr = a.x_r + (size_t)b * traj;
+  const float* xb = a.x_bar + (size_t)b * traj;
+  const double inv = 1.0 / (double)a.sigma_r;
   double s = 0.0;
-  for (int i = lo + threadIdx.x; i < hi; i += blockDim.x) {
-    const double d = ((double)a.x_r[(size_t)b * traj + i] - (double)a.x_bar[(size_t)b * traj + i]) /
-                     (double)a.sigma_r;
+  for (int i = c0 + threadIdx.x; i < c1; i += blockDim.x) {
+    const double d = ((double)xr[i] - (double)xb[i]) * inv;
     s += d * d;
   }
   s = block_sum_d(s, sh);
-  if (threadIdx.x == 0) a.rms[b * 2 + br] = hi > lo ? sqrt(s / (double)(hi - lo)) : 0.0;
+  if (threadIdx.x == 0) a.partial[(size_t)sb * kRemapChunks + blockIdx.x] = s;
+}
+
+__global__ void remap_finish_kernel(RemapArgs a) {
+  const int sb = blockIdx.x * blockDim.x + threadIdx.x;
+  if (sb >= a.B * 2) return;
+  const int br = sb % 2;
+  const int n = br == 0 ? a.Nv * a.Cv : a.Na * a.A;
+  double s = 0.0;
+  for (int c = 0; c < kRemapChunks; ++c) s += a.partial[(size_t)sb * kRemapChunks + c];
+  a.rms[sb] = n > 0 ? sqrt(s / (double)n) : 0.0;
 }
 
 // x[j] = x_bar[j+shift] + sigma_b0 d[j+shift] on mapped slots, sigma_b0 eps[j] elsewhere
@@ -961,7 +980,8 @@ hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t 
 }
 
 hipError_t launch_remap(const RemapArgs& a, hipStream_t s) {
-  launch_k(remap_rms_kernel, a.B * 2, 256, 0, s, a);
+  launch_k(remap_partial_kernel, dim3(kRemapChunks, a.B * 2), 256, 0, s, a);
+  launch_k(remap_finish_kernel, 1, 64, 0, s, a);
   const int64_t n = (int64_t)a.B * (a.Nv * a.Cv + a.Na * a.A);
   launch_k(remap_apply_kernel, (unsigned)((n + 255) / 256), 256, 0, s, a);
   return hipGetLastError();

@@ -193,7 +193,7 @@ WsLayout ws_layout(const Dims& d) {
   w.v = take(tr); w.x_bar = take(tr); w.x_r = take(tr); w.x_init = take(tr); w.x_work = take(tr);
   w.rr_rows = take((size_t)d.M * 3 * 8);
   w.rr_res = take((size_t)d.B * 2 * 8 * 8);
-  w.tr_rms = take((size_t)d.B * 2 * 8);
+  w.tr_rms = take((size_t)d.B * 2 * (1 + kRemapChunks) * 8);  // rms, then the run sums
   w.or_sums = take(WAM_MAX_COMPONENTS * 8);
   size_t split = 0;
   if (d.bf) {
@@ -240,6 +240,9 @@ struct wam_handle {
   int mod_k = 0;
   bool has_prev = false;
   int kappa = 0;
+  // the condition the retained denoising state continues under (cond_buf):
+  // set by WAM_ADAPT_REBIND and by every replan (its real condition)
+  bool cond_bound = false;
   double* host_stage = nullptr;  // pinned, small
   std::string err;
   ProfSlot prof[WAM_KC_COUNT];
@@ -689,14 +692,45 @@ int read_history(wam_t h, int k_from, int k_to, const wam_rr_profile* rr, wam_st
 
 int check_step(wam_t h, int k, const void* x, const void* cond) {
   if (!h) return WAM_E_ARG;
+  if (h->pend.begun)
+    return fail(h, WAM_E_STATE, "a replan is open (wam_replan_begin without wam_replan_end)");
   if (h->K <= 0) return fail(h, WAM_E_STATE, "schedule not set (wam_set_schedule)");
   if (k < 0 || k >= h->K) return fail(h, WAM_E_ARG, "step index out of range");
-  if (!x || (!cond && h->d.No > 0)) return fail(h, WAM_E_ARG, "null trajectory or condition pointer");
+  if (!x) return fail(h, WAM_E_ARG, "null trajectory pointer");
+  if (!cond && h->d.No > 0) return fail(h, WAM_E_ARG, "null condition pointer and no bound condition");
   return WAM_OK;
 }
 
 int copy_traj(wam_t h, float* dst, const float* src) {
   HIPCHK(h, hipMemcpyAsync(dst, src, (size_t)h->d.B * h->d.traj * 4, hipMemcpyDeviceToDevice, h->stream));
+  return WAM_OK;
+}
+
+// Observation Rebinding's rebinding step (Sec. 3.2): the retained denoising
+// state continues under the condition cond, which is copied into the
+// handle's condition buffer (stream-ordered).  Nothing else of the retained
+// state changes; the layer state persists across the rebinding (Sec. 3.3).
+int bind_condition(wam_t h, const float* cond) {
+  const Dims& d = h->d;
+  float* cb = h->S(h->ws.cond_buf);
+  if (d.No > 0 && cond != cb)
+    HIPCHK(h, launch_copy_f32(cond, cb, (int64_t)d.B * d.No * d.Co, h->stream));
+  h->cond_bound = true;
+  return WAM_OK;
+}
+
+// A null condition pointer in the step calls means the bound condition.
+const float* resolve_cond(wam_t h, const float* cond) {
+  if (cond || h->d.No == 0) return cond;
+  return h->cond_bound ? h->S(h->ws.cond_buf) : nullptr;
+}
+
+// Calls that read or write the retained state while a replan is open
+// (between wam_replan_begin and wam_replan_end) would interleave with the
+// enqueued anticipatory prefix; they are refused.
+int check_not_pending(wam_t h) {
+  if (h->pend.begun)
+    return fail(h, WAM_E_STATE, "a replan is open (wam_replan_begin without wam_replan_end)");
   return WAM_OK;
 }
 
@@ -901,6 +935,7 @@ const char* wam_last_error(wam_t h) { return h ? h->err.c_str() : "null handle";
 
 int wam_set_option(wam_t h, int option, int value) {
   if (!h) return WAM_E_ARG;
+  if (int st_ = check_not_pending(h)) return st_;
   switch (option) {
     case WAM_OPT_DEVICE_DECISION:
       if (!value && h->use_graphs) return fail(h, WAM_E_STATE, "graphs need the device decision");
@@ -924,6 +959,7 @@ int wam_set_option(wam_t h, int option, int value) {
 
 int wam_set_schedule(wam_t h, const float* sigmas, int K) {
   if (!h) return WAM_E_ARG;
+  if (int st_ = check_not_pending(h)) return st_;
   if (!sigmas || K < 1 || K > WAM_MAX_STEPS) return fail(h, WAM_E_ARG, "need 1 <= K <= WAM_MAX_STEPS");
   for (int i = 0; i < K; ++i)
     if (!(sigmas[i + 1] < sigmas[i])) return fail(h, WAM_E_ARG, "sigmas must decrease strictly");
@@ -936,6 +972,7 @@ int wam_set_schedule(wam_t h, const float* sigmas, int K) {
 
 int wam_velocity(wam_t h, int k, const float* x, const float* cond, float* v_out, const wam_rr_profile* rr,
                  wam_step_info* info) {
+  if (h) cond = resolve_cond(h, cond);
   int st = check_step(h, k, x, cond);
   if (st) return st;
   if (!v_out) return fail(h, WAM_E_ARG, "null v_out");
@@ -945,6 +982,7 @@ int wam_velocity(wam_t h, int k, const float* x, const float* cond, float* v_out
 }
 
 int wam_denoise_step(wam_t h, int k, float* x, const float* cond, const wam_rr_profile* rr, wam_step_info* info) {
+  if (h) cond = resolve_cond(h, cond);
   int st = check_step(h, k, x, cond);
   if (st) return st;
   if ((st = check_rr(h, rr))) return st;
@@ -955,15 +993,20 @@ int wam_denoise_step(wam_t h, int k, float* x, const float* cond, const wam_rr_p
 int wam_continue(wam_t h, int k_from, int k_to, float* x, const float* cond, const wam_rr_profile* rr,
                  int capture_stage, float* x_capture, wam_step_info* infos) {
   if (!h) return WAM_E_ARG;
+  cond = resolve_cond(h, cond);
+  int st0 = check_not_pending(h);
+  if (st0) return st0;
   if (h->K <= 0) return fail(h, WAM_E_STATE, "schedule not set (wam_set_schedule)");
   if (k_from < 0 || k_to > h->K || k_from > k_to) return fail(h, WAM_E_ARG, "need 0 <= k_from <= k_to <= K");
-  if (!x || (!cond && h->d.No > 0)) return fail(h, WAM_E_ARG, "null trajectory or condition pointer");
+  if (!x) return fail(h, WAM_E_ARG, "null trajectory pointer");
+  if (!cond && h->d.No > 0) return fail(h, WAM_E_ARG, "null condition pointer and no bound condition");
   int st = check_rr(h, rr);
   if (st) return st;
   return continue_impl(h, k_from, k_to, x, cond, rr, capture_stage, x_capture, infos);
 }
 
 int wam_hidden(wam_t h, int k, const float* x, const float* cond, int n_layers, float* h_out) {
+  if (h) cond = resolve_cond(h, cond);
   int st = check_step(h, k, x, cond);
   if (st) return st;
   if (!h_out || n_layers < 0 || n_layers > h->d.L) return fail(h, WAM_E_ARG, "need 0 <= n_layers <= L");
@@ -977,6 +1020,10 @@ int wam_hidden(wam_t h, int k, const float* x, const float* cond, int n_layers, 
 int wam_adapt_state(wam_t h, int op, const void* args) {
   if (!h) return WAM_E_ARG;
   const Dims& d = h->d;
+  if (op != WAM_ADAPT_RESET_ALL) {
+    int st = check_not_pending(h);
+    if (st) return st;
+  }
   switch (op) {
     case WAM_ADAPT_REMAP: {
       const wam_remap_args* a = static_cast<const wam_remap_args*>(args);
@@ -985,10 +1032,16 @@ int wam_adapt_state(wam_t h, int op, const void* args) {
       if (!(a->sigma_b0 >= 0.f)) return fail(h, WAM_E_ARG, "sigma_b0 must be >= 0");
       if (a->shift_action < 0 || a->shift_video < 0) return fail(h, WAM_E_ARG, "shifts must be >= 0");
       if (a->x_out == a->x_bar || a->x_out == a->x_r) return fail(h, WAM_E_ARG, "x_out must not alias inputs");
-      RemapArgs r{a->x_bar, a->x_r, a->noise, a->x_out, h->S<double>(h->ws.tr_rms), a->sigma_r, a->sigma_b0,
+      RemapArgs r{a->x_bar, a->x_r, a->noise, a->x_out, h->S<double>(h->ws.tr_rms),
+                  h->S<double>(h->ws.tr_rms) + 2 * d.B, a->sigma_r, a->sigma_b0,
                   a->shift_action, a->shift_video, d.B, d.Nv, d.Cv, d.Na, d.A};
       HIPCHK(h, launch_remap(r, h->stream));
       return WAM_OK;
+    }
+    case WAM_ADAPT_REBIND: {
+      const wam_rebind_args* a = static_cast<const wam_rebind_args*>(args);
+      if (!a || (!a->cond && d.No > 0)) return fail(h, WAM_E_ARG, "null rebind condition");
+      return bind_condition(h, a->cond);
     }
     case WAM_ADAPT_RESET_LAYER:
       h->layer_valid = false;
@@ -997,6 +1050,7 @@ int wam_adapt_state(wam_t h, int op, const void* args) {
       h->layer_valid = false;
       h->has_prev = false;
       h->kappa = 0;
+      h->cond_bound = false;
       h->pend.begun = false;
       return WAM_OK;
     case WAM_ADAPT_SET_REPLAN: {
@@ -1017,6 +1071,7 @@ int wam_adapt_state(wam_t h, int op, const void* args) {
 int wam_consistency_score(wam_t h, int n, const float* const* u_hat, const float* const* u, const int64_t* cnt,
                           const double* delta, const double* weight, double* S_out) {
   if (!h) return WAM_E_ARG;
+  if (int st_ = check_not_pending(h)) return st_;
   if (n < 1 || n > WAM_MAX_COMPONENTS || !u_hat || !u || !cnt || !delta || !weight || !S_out)
     return fail(h, WAM_E_ARG, "bad consistency-score arguments");
   double wsum = 0.0;
@@ -1087,10 +1142,10 @@ int run_segment(wam_t h, const wam_replan_args* a, int k0, int k1, const float* 
                 bool read_back) {
   const Dims& d = h->d;
   const wam_rr_profile* rr = (rr_allowed && a->rr.mode != WAM_RR_OFF) ? &a->rr : nullptr;
-  if (h->use_graphs) {  // captured steps read the condition from the staging buffer
-    float* cb = h->S(h->ws.cond_buf);
-    HIPCHK(h, launch_copy_f32(cond, cb, (int64_t)d.B * d.No * d.Co, h->stream));
-    cond = cb;
+  if (h->use_graphs) {  // captured steps read the condition from the handle's buffer
+    int st = bind_condition(h, cond);
+    if (st) return st;
+    cond = h->S(h->ws.cond_buf);
   }
   int st = continue_impl(h, k0, k1, h->S(h->ws.x_work), cond, rr, a->r, h->S(h->ws.x_r),
                          h->pend.steps + h->pend.nsteps, read_back);
@@ -1124,6 +1179,7 @@ int wam_replan_begin(wam_t h, const wam_replan_args* a) {
   float* x_init = h->S(h->ws.x_init);
   if (a->tr_enabled) {
     RemapArgs r{h->S(h->ws.x_bar), h->S(h->ws.x_r), a->noise_remap, x_init, h->S<double>(h->ws.tr_rms),
+                h->S<double>(h->ws.tr_rms) + 2 * d.B,
                 h->sigmas[a->r], h->sigmas[a->b0], a->shift_action, a->shift_video, d.B, d.Nv, d.Cv, d.Na, d.A};
     HIPCHK(h, launch_remap(r, h->stream));
   } else {
@@ -1164,7 +1220,9 @@ int wam_replan_end(wam_t h, const wam_replan_args* a, wam_replan_info* info) {
       h->kappa += 1;
       inf->n_bind = 1;
       inf->path = WAM_PATH_ACCEPT;
-      if ((st = run_segment(h, a, p.entry + a->k1, K, a->cond_real, a->rr_prefix, true))) return st;
+      if ((st = bind_condition(h, a->cond_real))) return st;
+      if ((st = run_segment(h, a, p.entry + a->k1, K, resolve_cond(h, nullptr), a->rr_prefix, true)))
+        return st;
     } else {
       h->kappa = 0;
       inf->path = WAM_PATH_REJECT;
@@ -1179,6 +1237,7 @@ int wam_replan_end(wam_t h, const wam_replan_args* a, wam_replan_info* info) {
   }
   if ((st = copy_traj(h, h->S(h->ws.x_bar), xw))) return st;
   if ((st = copy_traj(h, a->x_out, xw))) return st;
+  if (inf->path != WAM_PATH_ACCEPT && (st = bind_condition(h, a->cond_real))) return st;
   h->has_prev = true;
   inf->kappa = h->kappa;
   inf->steps = p.nsteps;
@@ -1203,6 +1262,7 @@ int wam_replan(wam_t h, const wam_replan_args* a, wam_replan_info* info) {
 
 int wam_get_replan_state(wam_t h, float* xb, float* xr, int32_t* kappa) {
   if (!h) return WAM_E_ARG;
+  if (int st_ = check_not_pending(h)) return st_;
   if (!h->has_prev) return fail(h, WAM_E_STATE, "no replan state yet");
   int st;
   if (xb && (st = copy_traj(h, xb, h->S(h->ws.x_bar)))) return st;

@@ -265,9 +265,11 @@ hipError_t launch_pack_condition(const float* obs, int n_obs, int c_obs, const f
 hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t s);
 
 // Trajectory Remapping
+constexpr int kRemapChunks = 64;  // runs per (sample, branch) of the remap rms sums
 struct RemapArgs {
   const float* x_bar; const float* x_r; const float* noise; float* x_out;
-  double* rms;  // [B][2] scratch
+  double* rms;      // [B][2] scratch
+  double* partial;  // [B][2][kRemapChunks] scratch
   float sigma_r, sigma_b0;
   int shift_action, shift_video;
   int B, Nv, Cv, Na, A;

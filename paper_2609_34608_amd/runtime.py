@@ -199,6 +199,13 @@ class WamModel:
         self._leave()
         return x_out
 
+    def rebind(self, cond):
+        """Observation Rebinding's rebinding step (WAM_ADAPT_REBIND): the retained
+        state continues under cond; cond=None in later step calls means it."""
+        self._enter()
+        a = abi.WamRebindArgs(cond=_ptr(cond))
+        self._check(self.lib.wam_adapt_state(self.h, abi.WAM_ADAPT_REBIND, C.byref(a)), "wam_adapt_state(REBIND)")
+
     def reset_layer_state(self):
         self._check(self.lib.wam_adapt_state(self.h, abi.WAM_ADAPT_RESET_LAYER, None), "RESET_LAYER")
 

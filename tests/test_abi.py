@@ -100,3 +100,16 @@ def test_single_branch_configs_accepted(lib, one_branch):
     assert lib.wam_host_weight_count(C.byref(cfg)) > 0
     assert lib.wam_workspace_bytes(C.byref(cfg)) > 0
     assert lib.wam_traj_elems(C.byref(cfg)) == base["Nv"] * 16 + base["Na"] * 7
+
+
+def test_binding_constants_match_header():
+    """Every WAM_* integer constant of include/wam.h has the same value in
+    the Python binding."""
+    text = open(HEADER).read()
+    defs = dict(re.findall(r"#define\s+(WAM_[A-Z0-9_]+)\s+\(?(-?\d+)\)?", text))
+    assert len(defs) >= 40
+    for name, val in defs.items():
+        if hasattr(L, name):
+            assert getattr(L, name) == int(val), name
+    for name in ("WAM_ADAPT_REBIND", "WAM_E_STATE", "WAM_RR_SINGLE", "WAM_ATTN_PLAIN", "WAM_KC_COUNT"):
+        assert getattr(L, name) == int(defs[name])

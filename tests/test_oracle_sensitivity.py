@@ -103,3 +103,33 @@ def test_threaded_attention_equals_serial():
     finally:
         OD.ATTENTION_THREADS = old
     np.testing.assert_array_equal(serial, threaded)
+
+
+def test_small_model_injection_quantity():
+    """The residual-injection check at the small model's shape compares the
+    velocity change that reuse makes (forced reuse minus full computation on
+    the same latent) at tolerance 2e-2.  Dropping the retained residual R_a,
+    or injecting p_a in its place, moves that change by at least ten times
+    the tolerance."""
+    spec = get_workload("small")
+    W = make_weights(spec)
+    sig = OM.flow_schedule(spec.K).astype(np.float32).astype(np.float64)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    prof = OM.RRProfile(*spec.rr_bounds, mode=OM.RR_FORCE_SKIP)
+    st = OM.LayerState()
+    v0, _ = OM.velocity_rr(W, spec, x0, cond, sig[0], prof, st)
+    x1 = OM.euler_update(x0, v0, sig[0], sig[1])
+    vf = OD.velocity(W, spec, x1, cond, sig[1])
+
+    def skip_with(R_a):
+        s = OM.LayerState()
+        s.p_a, s.R_a = st.p_a, R_a
+        v, info = OM.velocity_rr(W, spec, x1, cond, sig[1], prof, s)
+        assert info.accepted
+        return v - vf
+
+    ref = skip_with(st.R_a)
+    for what, R_a in (("zero R_a", np.zeros_like(st.R_a)), ("p_a for R_a", st.p_a)):
+        moved = _rel(skip_with(R_a), ref)
+        assert moved >= 10 * 2e-2, (what, moved)
