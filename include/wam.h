@@ -358,6 +358,24 @@ int wam_replan_end(wam_t h, const wam_replan_args *args, wam_replan_info *info);
 /* Copies of the retained replan state (device [B][traj] each; may be NULL). */
 int wam_get_replan_state(wam_t h, float *x_bar, float *x_r, int32_t *kappa);
 
+/* Trajectory Remapping that allocates nothing, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same computation and kernels as
+ * wam_adapt_state(WAM_ADAPT_REMAP), without a handle.  From cfg only B, Nv,
+ * Cv, Na and A are read (1 <= B <= WAM_MAX_BATCH, Nv, Na >= 0, Nv + Na >= 1,
+ * Cv, A >= 1, B * traj < 2^31); args as for WAM_ADAPT_REMAP (device buffers,
+ * caller-owned).  Enqueued on hip_stream (NULL: the default stream) with no
+ * synchronisation.  The reduction scratch (at most WAM_MAX_BATCH x 2 x 65
+ * float64, 16.6 KB) is a static array of the library on each GPU, held until
+ * the process ends; every call on one GPU shares it, so calls that overlap on
+ * one GPU (different streams or threads) race.  The call makes no device
+ * allocation and no hipMalloc / hipFree.  Errors: WAM_E_SHAPE for sizes
+ * beyond those limits, WAM_E_ARG for invalid arguments, WAM_E_HIP for a
+ * runtime error; wam_noalloc_last_error() returns this thread's message of
+ * the last failing call. */
+int wam_remap_noalloc(const wam_config *cfg, const wam_remap_args *args, void *hip_stream);
+const char *wam_noalloc_last_error(void);
+
 /* ---- measurement ------------------------------------------------------------ */
 /* Time every launch of kernel class kc (WAM_KC_*), up to max_launches
  * launches: a HIP event pair per launch, stamped by the dispatches themselves

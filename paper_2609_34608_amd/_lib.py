@@ -113,6 +113,8 @@ EXPORTS = {
     "wam_profile_enable": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int]),
     "wam_profile_read": (C.c_int, [C.c_void_p, C.c_int, C.POINTER(C.c_double), C.POINTER(C.c_int64),
                                    C.POINTER(C.c_double)]),
+    "wam_remap_noalloc": (C.c_int, [C.POINTER(WamConfig), C.POINTER(WamRemapArgs), C.c_void_p]),
+    "wam_noalloc_last_error": (C.c_char_p, []),
     "wam_probe_mfma_bf16": (C.c_int, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_void_p, C.POINTER(C.c_double),
                                       C.POINTER(C.c_double)]),
     "wam_probe_copy": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t, C.c_int, C.POINTER(C.c_double),

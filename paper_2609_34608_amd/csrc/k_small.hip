@@ -2,6 +2,9 @@
 // state-adaptation operators (gfx950, wave64).
 #include <math.h>
 
+#include <mutex>
+#include <string>
+
 #include "wam_internal.h"
 
 namespace wam {
@@ -1003,3 +1006,82 @@ hipError_t launch_or_sums(int n_comp, const float* const* u_hat, const float* co
 }
 
 }  // namespace wam
+
+// ================================================================ no-alloc remap
+// Trajectory Remapping for callers that cannot allocate device memory (code
+// under graph capture, tight serving loops): the rms and run-sum scratch of
+// the remap kernels lives in this file-scope device array instead of a
+// workspace.  Each GPU holds its own copy until the process ends; its device
+// address is looked up once per device (with that device current) and only
+// that address is ever handed to kernels or copies.
+namespace wam {
+namespace {
+
+constexpr int kNoAllocScratchDoubles = WAM_MAX_BATCH * 2 * (1 + kRemapChunks);  // 16.6 KB
+constexpr int kMaxDevices = 64;
+
+__device__ __align__(256) double scratch[kNoAllocScratchDoubles];
+
+std::mutex g_scratch_mu;
+double* g_scratch_ptr[kMaxDevices] = {};
+
+thread_local std::string t_noalloc_err;
+
+int noalloc_fail(int code, const char* msg) {
+  t_noalloc_err = msg;
+  return code;
+}
+
+// Device address of this GPU's copy of `scratch` (looked up on first use).
+int scratch_for_current_device(double** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return noalloc_fail(WAM_E_HIP, "wam_remap_noalloc: no current device");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p)
+      return noalloc_fail(WAM_E_HIP, "wam_remap_noalloc: hipGetSymbolAddress of the scratch array failed");
+    g_scratch_ptr[dev] = static_cast<double*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return WAM_OK;
+}
+
+}  // namespace
+}  // namespace wam
+
+extern "C" {
+
+const char* wam_noalloc_last_error(void) { return wam::t_noalloc_err.c_str(); }
+
+int wam_remap_noalloc(const wam_config* cfg, const wam_remap_args* a, void* hip_stream) {
+  using namespace wam;
+  if (!cfg || !a) return noalloc_fail(WAM_E_ARG, "wam_remap_noalloc: null argument");
+  if (cfg->B < 1 || cfg->B > WAM_MAX_BATCH)
+    return noalloc_fail(WAM_E_SHAPE, "wam_remap_noalloc: batch must be 1..WAM_MAX_BATCH (16): the static "
+                                     "scratch holds 16 x 2 x 65 float64 sums");
+  if (cfg->Nv < 0 || cfg->Na < 0 || cfg->Cv < 1 || cfg->A < 1 || cfg->Nv + cfg->Na < 1)
+    return noalloc_fail(WAM_E_SHAPE, "wam_remap_noalloc: need Nv, Na >= 0, Nv + Na >= 1, Cv, A >= 1");
+  const int64_t traj = (int64_t)cfg->Nv * cfg->Cv + (int64_t)cfg->Na * cfg->A;
+  if (traj * cfg->B > (int64_t)INT32_MAX)
+    return noalloc_fail(WAM_E_SHAPE, "wam_remap_noalloc: B * traj must fit in 31 bits");
+  if (!a->x_bar || !a->x_r || !a->noise || !a->x_out)
+    return noalloc_fail(WAM_E_ARG, "wam_remap_noalloc: null remap argument");
+  if (!(a->sigma_r > 0.f)) return noalloc_fail(WAM_E_ARG, "wam_remap_noalloc: sigma_r must be > 0");
+  if (!(a->sigma_b0 >= 0.f)) return noalloc_fail(WAM_E_ARG, "wam_remap_noalloc: sigma_b0 must be >= 0");
+  if (a->shift_action < 0 || a->shift_video < 0)
+    return noalloc_fail(WAM_E_ARG, "wam_remap_noalloc: shifts must be >= 0");
+  if (a->x_out == a->x_bar || a->x_out == a->x_r)
+    return noalloc_fail(WAM_E_ARG, "wam_remap_noalloc: x_out must not alias inputs");
+  double* sc = nullptr;
+  int st = scratch_for_current_device(&sc);
+  if (st) return st;
+  RemapArgs r{a->x_bar, a->x_r, a->noise, a->x_out, sc, sc + 2 * cfg->B, a->sigma_r, a->sigma_b0,
+              a->shift_action, a->shift_video, cfg->B, cfg->Nv, cfg->Cv, cfg->Na, cfg->A};
+  if (launch_remap(r, static_cast<hipStream_t>(hip_stream)) != hipSuccess)
+    return noalloc_fail(WAM_E_HIP, "wam_remap_noalloc: kernel launch failed");
+  return WAM_OK;
+}
+
+}  // extern "C"

@@ -334,6 +334,21 @@ class IdmPair:
         return iv, ia
 
 
+def remap_noalloc(cfg: abi.WamConfig, x_bar, x_r, sigma_r, sigma_b0, shift_action, shift_video, noise, x_out,
+                  stream: torch.cuda.Stream | None = None):
+    """Trajectory Remapping without a handle or workspace (wam_remap_noalloc);
+    enqueued on stream (default: torch's current stream on x_out's device)."""
+    lib = abi.lib()
+    s = stream if stream is not None else torch.cuda.current_stream(x_out.device)
+    a = abi.WamRemapArgs(x_bar=_ptr(x_bar), x_r=_ptr(x_r), sigma_r=sigma_r, sigma_b0=sigma_b0,
+                         shift_action=shift_action, shift_video=shift_video, noise=_ptr(noise), x_out=_ptr(x_out))
+    rc = lib.wam_remap_noalloc(C.byref(cfg), C.byref(a), C.c_void_p(s.cuda_stream))
+    if rc != abi.WAM_OK:
+        raise WamError(f"wam_remap_noalloc: {lib.wam_status_string(rc).decode()}: "
+                       f"{lib.wam_noalloc_last_error().decode()}")
+    return x_out
+
+
 def probe_mfma_bf16(shape: int = 0, n_blocks: int = 1024, iters: int = 20000, device="cuda:0"):
     """Achievable bf16 MFMA rate (wam_probe_mfma_bf16): returns (TFLOP/s, ms)."""
     lib = abi.lib()
