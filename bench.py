@@ -109,6 +109,76 @@ def summarize_pmc(fetch_csv, write_csv, probe_mb, workload, commands):
     print(json.dumps({k: round(v["traffic_bytes"]) for k, v in classes.items()}))
 
 
+def class_flops(spec, cls: str) -> float:
+    """Algorithmic FLOP of one launch of a contraction class at a workload."""
+    M, D, F, T, B = spec.M, spec.D, spec.F, spec.T, spec.B
+    return {"gemm_qkv": 2.0 * M * D * 3 * D, "gemm_proj": 2.0 * M * D * D, "gemm_fc1": 2.0 * M * D * F,
+            "gemm_fc2": 2.0 * M * F * D, "attention": 4.0 * B * T * T * D}[cls]
+
+
+def summarize_mfma(pmc_csv, workload, commands, simds=1024, xcds=8):
+    """MFMA counters per contraction class from one rocprofv3 --pmc run
+    (SQ_INSTS_VALU_MFMA_MOPS_BF16, SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE,
+    SQ_BUSY_CU_CYCLES): bf16 MFMA FLOP counted by the hardware against the
+    algorithmic FLOP, MFMA-busy fraction of the SIMDs over the dispatch, and
+    the shader clock implied by GRBM_GUI_ACTIVE over the dispatch time.
+    rocprofv3 reports GRBM_GUI_ACTIVE summed over the 8 XCDs (each has its own
+    graphics block), so one XCD's active cycles are the value / 8."""
+    from synth import get_workload
+    spec = get_workload(workload)
+    per = {}
+    with open(pmc_csv) as f:
+        for r in csv.DictReader(f):
+            cls = kernel_class(r["Kernel_Name"])
+            if cls is None or not cls.startswith(("gemm", "attention")):
+                continue
+            d = per.setdefault(cls, {}).setdefault(r["Dispatch_Id"], {"name": r["Kernel_Name"]})
+            d[r["Counter_Name"]] = float(r["Counter_Value"])
+            d["ns"] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    rows = []
+    for cls in CLASS_NAMES:
+        if cls not in per:
+            continue
+        ds = [d for d in per[cls].values() if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in d and "GRBM_GUI_ACTIVE" in d]
+        if not ds:
+            continue
+        n = len(ds)
+        avg = lambda k: sum(d[k] for d in ds) / n  # noqa: E731
+        ns = avg("ns")
+        flop_hw = avg("SQ_INSTS_VALU_MFMA_MOPS_BF16") * 512.0
+        flop_alg = class_flops(spec, cls)
+        active = avg("GRBM_GUI_ACTIVE") / xcds  # cycles of one XCD
+        busy = avg("SQ_VALU_MFMA_BUSY_CYCLES") / (active * simds)
+        clock = active / ns  # GHz
+        rows.append((cls, n, ns / 1e3, flop_alg / 1e9, flop_hw / 1e9, flop_hw / flop_alg,
+                     flop_alg / ns / 1e3, flop_alg / ns / 1e3 / MFMA_BF16_PEAK_TFLOPS, busy, clock,
+                     flop_hw / ns / 1e3 / (clock * 1e9 * simds * 1024 / 1e12)))
+    path = os.path.join(ROOT, "profiles", f"mfma_counters_{workload}.md")
+    with open(path, "w") as f:
+        f.write(f"# MFMA counters — {workload} workload (bench.py --workload {workload})\n\n")
+        f.write("Commands (repository root, one MI355X, after `cd /tmp && export TMPDIR=/tmp` for the "
+                "profiler's files):\n\n")
+        for c in commands:
+            f.write(f"    {c}\n")
+        f.write("\nPer contraction class, averaged over its dispatches (kernels serialised by the counter "
+                "collection):\n\n")
+        f.write("* hw GFLOP = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 (the bf16 MFMA work the hardware issued);\n"
+                "* alg GFLOP = the algorithmic work of one launch (2MNK; attention 4 B T^2 D);\n"
+                "* TFLOP/s and % of 2.5 PF = alg GFLOP / dispatch time;\n"
+                "* MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 x 1024 SIMDs) (rocprofv3 sums "
+                "GRBM_GUI_ACTIVE over the 8 XCDs);\n"
+                "* clock = GRBM_GUI_ACTIVE / 8 / dispatch time;\n"
+                "* issue at clock = hw FLOP / (time x clock x 1024 SIMDs x 1024 FLOP per SIMD-cycle), the "
+                "fraction of the dense bf16 rate at the measured clock.\n\n")
+        f.write("| class | dispatches | avg us | alg GFLOP | hw GFLOP | hw/alg | TFLOP/s | % of 2.5 PF | "
+                "MFMA busy | clock GHz | issue at clock |\n|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|---:|\n")
+        for r in rows:
+            f.write(f"| {r[0]} | {r[1]} | {r[2]:.2f} | {r[3]:.2f} | {r[4]:.2f} | {r[5]:.4f} | {r[6]:.1f} | "
+                    f"{100 * r[7]:.1f}% | {100 * r[8]:.1f}% | {r[9]:.3f} | {100 * r[10]:.1f}% |\n")
+        f.write(f"\nSource hash of the HIP kernels: `{source_hash()}`.\n")
+    print(open(path).read())
+
+
 def lookup_traffic(workload: str, cls: str):
     """Traffic per launch of a class from the committed PMC summary, or None
     when there is none or the kernels changed since the counters were taken."""
@@ -149,6 +219,9 @@ def parse():
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="write the per-class traffic summary of two --pmc runs and exit")
     p.add_argument("--pmc-command", action="append", default=[], help="command lines recorded in the summary")
+    p.add_argument("--summarize-mfma", metavar="PMC_CSV",
+                   help="write the MFMA-counter summary of one --pmc run (profiles/mfma_counters_<workload>.md) "
+                        "and exit")
     p.add_argument("--ablation", action="store_true",
                    help="closed-loop GPU time and observation-to-action latency per variant, then exit")
     p.add_argument("--diagnostics", action="store_true",
@@ -164,6 +237,9 @@ def main():
     if args.summarize_pmc:
         summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.copy_probe_mib, args.workload,
                       args.pmc_command)
+        return
+    if args.summarize_mfma:
+        summarize_mfma(args.summarize_mfma, args.workload, args.pmc_command)
         return
     if args.ablation:
         if args.gpus != 1:
