@@ -293,7 +293,7 @@ def achievable_peaks():
     return {"mfma_bf16_16x16x32_tflops": round(t16, 1), "mfma_bf16_32x32x16_tflops": round(t32, 1),
             "copy_gbs": round(gbs, 1),
             "method": "wam_probe_mfma_bf16 (1024 blocks x 4 waves, 20000 rounds of independent MFMA chains "
-                      "on register operands) and wam_probe_copy (1 GiB device copy, 16-byte accesses, read + "
+                      "on register operands) and wam_probe_copy (1 GiB device copy, one 16-byte element per thread, read + "
                       "write bytes counted), HIP events"}
 
 

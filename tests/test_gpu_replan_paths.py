@@ -184,3 +184,52 @@ def test_small_bf16_injection_matches_oracle(dev):
           f"alpha {info.alpha.ravel()}, cos {info.cos.ravel()}")
     assert e <= BF16_TOL, e
     assert ea <= 1e-2, ea
+
+
+@pytest.mark.parametrize("name", ["tiny_rr", "small"])
+def test_free_running_decision_agreement(dev, name):
+    """Decision-trace protocol, part (i): the oracle runs free (its own gate,
+    its own trajectory) beside the device over a whole chunk with Residual
+    Rescaling on, thresholds placed inside the range of the statistics so
+    that both decisions occur.  Reported: the agreement rate of the reuse
+    decisions and the margin of every flip (the oracle's distance of cos or
+    fit from its threshold); a flip is only allowed at a near-tie (margin
+    within 1e-2, the bf16 error of the statistics is about 1e-3)."""
+    from paper_2609_34608_amd import _lib as L
+    kw = dict(bias_std=0.02, gain_std=0.1) if name == "tiny_rr" else {}
+    spec, W, m = model_for(name, dev, **kw)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    x0 = make_initial_noise(spec)
+    cond = make_observations(spec, 0)[0]
+    # statistics of a pass that refreshes at every step (the gate never
+    # passes) set the thresholds: cos at its median, fit never binding
+    _, never_o = rr_of(spec, L.WAM_RR_AUTO, gamma_cos=1.5)
+    _, _, infos = OM.denoise(W, spec, x0, cond, sig, 0, spec.K, never_o, OM.LayerState())
+    cos_all = np.concatenate([i.cos.ravel() for i in infos if i.attempted])
+    fit_all = np.concatenate([i.fit.ravel() for i in infos if i.attempted])
+    g_cos = float(np.float32(np.median(cos_all)))
+    g_fit = float(np.float32(np.max(fit_all) * 1.01))
+    rr_g, rr_o = rr_of(spec, L.WAM_RR_AUTO, gamma_cos=g_cos, gamma_fit=g_fit)
+    m.reset_layer_state()
+    x = to_dev(x0, dev)
+    got = m.continue_(0, spec.K, x, to_dev(cond, dev), rr=rr_g)
+    _, _, ref = OM.denoise(W, spec, x0, cond, sig, 0, spec.K, rr_o, OM.LayerState())
+    n_att, agree, flips = 0, 0, []
+    for k, (g, r) in enumerate(zip(got, ref)):
+        if not (g.attempted and r.attempted):
+            assert g.attempted == r.attempted, k
+            continue
+        n_att += 1
+        if g.accepted == r.accepted:
+            agree += 1
+        else:
+            margin = float(min(np.min(np.abs(r.cos - g_cos)), np.min(np.abs(r.fit - g_fit))))
+            flips.append((k, margin))
+    rate = agree / max(n_att, 1)
+    print(f"{name}: free-running decision agreement {agree}/{n_att} = {rate:.3f}; gamma_cos {g_cos:.4f}; "
+          f"flips (step, margin): {flips}; device decisions {[int(g.accepted) for g in got if g.attempted]}, "
+          f"oracle {[int(r.accepted) for r in ref if r.attempted]}")
+    assert n_att >= 3
+    for k, margin in flips:
+        assert margin <= 1e-2, (k, margin)
