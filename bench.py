@@ -227,6 +227,9 @@ def parse():
     p.add_argument("--diagnostics", action="store_true",
                    help="state-continuity diagnostics (layer change, reuse output error, consecutive-replan "
                         "latent similarity, remapped-vs-native action RMSE), then exit")
+    p.add_argument("--sweep", action="store_true",
+                   help="bandwidth of Trajectory Remapping and the rebinding score at 2^22 .. 2^28 elements, "
+                        "then exit")
     p.add_argument("--window-ms", type=float, default=20.0,
                    help="simulated action-execution window between replans (ablation mode)")
     return p.parse_args()
@@ -252,6 +255,9 @@ def main():
         return
     if args.diagnostics:
         diagnostics(args)
+        return
+    if args.sweep:
+        sweep(args)
         return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); the library has no "
@@ -281,6 +287,62 @@ def main():
         out["replay"]["dominant_kernel"] = {k: r["roofline"][k]
                                             for k in ("kernel", "achieved", "frac", "avg_launch_us")}
     print(json.dumps(out), flush=True)
+
+
+def sweep(args):
+    """Trajectory Remapping (wam_remap_noalloc: rms runs, their sum, the
+    remapped initialisation) and the Observation Rebinding score
+    (wam_consistency_score: run sums on the device, their sum on the host)
+    over 2^22 .. 2^28 trajectory / condition elements, beside a plain copy of
+    the same size: the bandwidth of these operators once they are not
+    latency-bound.  Algorithmic bytes: remap 20 per element (the rms pass
+    reads x^r and x_bar, the remap reads them again and writes x; no slot is
+    shifted out, so no noise is read), score 8 (u_hat and u), copy 8."""
+    import numpy as np
+    import torch
+
+    from paper_2609_34608_amd import runtime as R
+    from synth import get_workload, make_weights
+    dev = torch.device("cuda:0")
+    tiny = get_workload("tiny")
+    m = R.WamModel(R.config_of(tiny), make_weights(tiny), device=dev)
+    rows = []
+    for lg in range(22, 29):
+        n = 1 << lg
+        spec = tiny.replace(B=1, Nv=n // 16, Cv=16, Na=0, A=1)
+        cfg = R.config_of(spec)
+        g = torch.Generator(device=dev).manual_seed(lg)
+        xb = torch.randn(1, n, device=dev, generator=g)
+        xr = torch.randn(1, n, device=dev, generator=g)
+        eps = torch.randn(1, n, device=dev, generator=g)
+        out = torch.empty_like(xb)
+        reps = 20
+        R.remap_noalloc(cfg, xb, xr, 0.6, 0.75, 0, 0, eps, out)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            R.remap_noalloc(cfg, xb, xr, 0.6, 0.75, 0, 0, eps, out)
+        e1.record()
+        e1.synchronize()
+        t_tr = e0.elapsed_time(e1) / reps
+        m.consistency_score([xb], [xr], [1.0], [1.0])
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            m.consistency_score([xb], [xr], [1.0], [1.0])
+        t_or = (time.perf_counter() - t0) / reps * 1e3
+        gbs_copy, t_cp = R.probe_copy(n * 4, reps=reps)
+        r = {"log2_elements": lg, "remap_us": round(1e3 * t_tr, 2),
+             "remap_GBs": round(20.0 * n / (t_tr * 1e-3) / 1e9, 1),
+             "score_us": round(1e3 * t_or, 2), "score_GBs": round(8.0 * n / (t_or * 1e-3) / 1e9, 1),
+             "copy_us": round(1e3 * t_cp, 2), "copy_GBs": round(gbs_copy, 1)}
+        r["remap_frac_hbm"] = round(r["remap_GBs"] / HBM_PEAK_GBS, 4)
+        r["score_frac_hbm"] = round(r["score_GBs"] / HBM_PEAK_GBS, 4)
+        rows.append(r)
+        print(json.dumps(r), flush=True)
+        del xb, xr, eps, out
+    m.close()
+    print(json.dumps({"sweep": rows}), flush=True)
 
 
 def achievable_peaks():

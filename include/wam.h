@@ -365,8 +365,8 @@ int wam_get_replan_state(wam_t h, float *x_bar, float *x_r, int32_t *kappa);
  * Cv, Na and A are read (1 <= B <= WAM_MAX_BATCH, Nv, Na >= 0, Nv + Na >= 1,
  * Cv, A >= 1, B * traj < 2^31); args as for WAM_ADAPT_REMAP (device buffers,
  * caller-owned).  Enqueued on hip_stream (NULL: the default stream) with no
- * synchronisation.  The reduction scratch (at most WAM_MAX_BATCH x 2 x 65
- * float64, 16.6 KB) is a static array of the library on each GPU, held until
+ * synchronisation.  The reduction scratch (at most WAM_MAX_BATCH x 2 x 1025
+ * float64, 256.3 KiB) is a static array of the library on each GPU, held until
  * the process ends; every call on one GPU shares it, so calls that overlap on
  * one GPU (different streams or threads) race.  The call makes no device
  * allocation and no hipMalloc / hipFree.  Errors: WAM_E_SHAPE for sizes

@@ -2,6 +2,7 @@
 // state-adaptation operators (gfx950, wave64).
 #include <math.h>
 
+#include <algorithm>
 #include <mutex>
 #include <string>
 
@@ -748,24 +749,43 @@ __global__ __launch_bounds__(256) void copy_f32x4_kernel(const f32x4* __restrict
 
 // ------------------------------------------------------------- Trajectory Remapping
 // rms of (x^r - x_bar)/sigma_r per (sample, branch) over the whole branch, in
-// two launches: each branch is cut into kRemapChunks equal runs, one block
-// per run sums its squares (float64), then one thread per (sample, branch)
-// adds the run sums in run order (the same bits on every call).
+// two launches: each branch is cut into reduce_chunks(n) equal runs, one block
+// per run sums its squares (float64); then one block per (sample, branch)
+// adds the run sums in a fixed order (the same bits on every call) and turns
+// the rms into the remap coefficient sigma_b0 / (sigma_r rms) (0 for a zero
+// direction).
 __global__ __launch_bounds__(256) void remap_partial_kernel(RemapArgs a) {
   __shared__ double sh[16];
   const int sb = blockIdx.y;  // sample * 2 + branch
   const int b = sb / 2, br = sb % 2;
-  const int traj = a.Nv * a.Cv + a.Na * a.A;
-  const int lo = br == 0 ? 0 : a.Nv * a.Cv;
-  const int hi = br == 0 ? a.Nv * a.Cv : traj;
-  const int per = (hi - lo + kRemapChunks - 1) / kRemapChunks;
-  const int c0 = lo + (int)blockIdx.x * per;
-  const int c1 = min(c0 + per, hi);
+  const int64_t traj = (int64_t)a.Nv * a.Cv + (int64_t)a.Na * a.A;
+  const int64_t lo = br == 0 ? 0 : (int64_t)a.Nv * a.Cv;
+  const int64_t hi = br == 0 ? (int64_t)a.Nv * a.Cv : traj;
+  const int nch = reduce_chunks(hi - lo);
+  if ((int)blockIdx.x >= nch) return;
+  const int64_t per = (hi - lo + nch - 1) / nch;
+  const int64_t c0 = lo + (int64_t)blockIdx.x * per;
+  const int64_t c1 = c0 + per < hi ? c0 + per : hi;
   const float* xr = a.x_r + (size_t)b * traj;
   const float* xb = a.x_bar + (size_t)b * traj;
   const double inv = 1.0 / (double)a.sigma_r;
   double s = 0.0;
-  for (int i = c0 + threadIdx.x; i < c1; i += blockDim.x) {
+  int64_t i = c0 + threadIdx.x;
+  // eight elements per thread in flight, then the remainder
+  for (; i + 7 * 256 < c1; i += 8 * 256) {
+    float r[8], x[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      r[u] = xr[i + u * 256];
+      x[u] = xb[i + u * 256];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const double d = ((double)r[u] - (double)x[u]) * inv;
+      s += d * d;
+    }
+  }
+  for (; i < c1; i += 256) {
     const double d = ((double)xr[i] - (double)xb[i]) * inv;
     s += d * d;
   }
@@ -773,39 +793,49 @@ __global__ __launch_bounds__(256) void remap_partial_kernel(RemapArgs a) {
   if (threadIdx.x == 0) a.partial[(size_t)sb * kRemapChunks + blockIdx.x] = s;
 }
 
-__global__ void remap_finish_kernel(RemapArgs a) {
-  const int sb = blockIdx.x * blockDim.x + threadIdx.x;
-  if (sb >= a.B * 2) return;
-  const int br = sb % 2;
-  const int n = br == 0 ? a.Nv * a.Cv : a.Na * a.A;
+// Fixed-order sum of run sums p[0 .. n): thread t adds runs t, t + 256, ...
+// in turn, then the 256 thread sums combine as block_sum_d does.
+__device__ __forceinline__ double runs_sum(const double* p, int n, double* sh) {
   double s = 0.0;
-  for (int c = 0; c < kRemapChunks; ++c) s += a.partial[(size_t)sb * kRemapChunks + c];
-  a.rms[sb] = n > 0 ? sqrt(s / (double)n) : 0.0;
+  for (int c = threadIdx.x; c < n; c += 256) s += p[c];
+  return block_sum_d(s, sh);
 }
 
-// x[j] = x_bar[j+shift] + sigma_b0 d[j+shift] on mapped slots, sigma_b0 eps[j] elsewhere
-__global__ void remap_apply_kernel(RemapArgs a) {
-  const int traj = a.Nv * a.Cv + a.Na * a.A;
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)a.B * traj) return;
-  const int b = (int)(idx / traj), i = (int)(idx % traj);
-  const int nv = a.Nv * a.Cv;
-  int br, slot, ch, nslot, width, shift, base;
-  if (i < nv) {
-    br = 0; slot = i / a.Cv; ch = i % a.Cv; nslot = a.Nv; width = a.Cv; shift = a.shift_video; base = 0;
-  } else {
-    br = 1; slot = (i - nv) / a.A; ch = (i - nv) % a.A; nslot = a.Na; width = a.A; shift = a.shift_action; base = nv;
+__global__ __launch_bounds__(256) void remap_finish_kernel(RemapArgs a) {
+  __shared__ double sh[16];
+  const int sb = blockIdx.x;
+  const int br = sb % 2;
+  const int64_t n = br == 0 ? (int64_t)a.Nv * a.Cv : (int64_t)a.Na * a.A;
+  const double s = runs_sum(a.partial + (size_t)sb * kRemapChunks, reduce_chunks(n), sh);
+  if (threadIdx.x == 0) {
+    // x = x_bar + sigma_b0 d with d = ((x^r - x_bar) / sigma_r) / rms
+    const double rms = n > 0 ? sqrt(s / (double)n) : 0.0;
+    a.coef[sb] = rms > 0.0 ? (double)a.sigma_b0 / ((double)a.sigma_r * rms) : 0.0;
   }
+}
+
+// x[j] = x_bar[j+shift] + sigma_b0 d[j+shift] on mapped slots, sigma_b0 eps[j]
+// elsewhere; one element per thread, grid (elements, sample).  Slot j of a
+// branch of width w is mapped when j + shift < slots, i.e. when the element
+// index within the branch plus shift * w stays inside the branch.
+__global__ __launch_bounds__(256) void remap_apply_kernel(RemapArgs a) {
+  const int64_t traj = (int64_t)a.Nv * a.Cv + (int64_t)a.Na * a.A;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= traj) return;
+  const int b = blockIdx.y;
+  const int64_t nv = (int64_t)a.Nv * a.Cv;
+  const bool video = i < nv;
+  const int64_t src = i + (video ? (int64_t)a.shift_video * a.Cv : (int64_t)a.shift_action * a.A);
+  const int64_t end = video ? nv : traj;
+  const size_t base = (size_t)b * traj;
   float out;
-  if ((int64_t)slot + shift < nslot) {
-    const size_t src = (size_t)b * traj + base + (size_t)(slot + shift) * width + ch;
-    const double rms = a.rms[b * 2 + br];
-    const double dir = rms > 0.0 ? (((double)a.x_r[src] - (double)a.x_bar[src]) / (double)a.sigma_r) / rms : 0.0;
-    out = (float)((double)a.x_bar[src] + (double)a.sigma_b0 * dir);
+  if (src < end) {
+    const double xb = (double)a.x_bar[base + src];
+    out = (float)(xb + ((double)a.x_r[base + src] - xb) * a.coef[b * 2 + (video ? 0 : 1)]);
   } else {
-    out = a.sigma_b0 * a.noise[idx];
+    out = a.sigma_b0 * a.noise[base + i];
   }
-  a.x_out[idx] = out;
+  a.x_out[base + i] = out;
 }
 
 // ------------------------------------------------------------- Observation Rebinding
@@ -817,16 +847,41 @@ struct OrSumArgs {
   double* sums;
 };
 
-__global__ void or_sums_kernel(OrSumArgs a) {
+// Run sums of ((u_hat - u) / delta)^2 of component blockIdx.y, run blockIdx.x
+// of reduce_chunks(n) (float64); the host adds the runs in order.
+__global__ __launch_bounds__(256) void or_sums_kernel(OrSumArgs a) {
   __shared__ double sh[16];
-  const int m = blockIdx.x;
+  const int m = blockIdx.y;
+  const int64_t n = a.n[m];
+  const int nch = reduce_chunks(n);
+  if ((int)blockIdx.x >= nch) return;
+  const int64_t per = (n + nch - 1) / nch;
+  const int64_t c0 = (int64_t)blockIdx.x * per;
+  const int64_t c1 = c0 + per < n ? c0 + per : n;
+  const float* uh = a.u_hat[m];
+  const float* uu = a.u[m];
+  const double idl = a.inv_delta[m];
   double s = 0.0;
-  for (int64_t i = threadIdx.x; i < a.n[m]; i += blockDim.x) {
-    const double r = ((double)a.u_hat[m][i] - (double)a.u[m][i]) * a.inv_delta[m];
+  int64_t i = c0 + threadIdx.x;
+  for (; i + 7 * 256 < c1; i += 8 * 256) {
+    float p[8], q[8];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      p[v] = uh[i + v * 256];
+      q[v] = uu[i + v * 256];
+    }
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      const double r = ((double)p[v] - (double)q[v]) * idl;
+      s += r * r;
+    }
+  }
+  for (; i < c1; i += 256) {
+    const double r = ((double)uh[i] - (double)uu[i]) * idl;
     s += r * r;
   }
   s = block_sum_d(s, sh);
-  if (threadIdx.x == 0) a.sums[m] = s;
+  if (threadIdx.x == 0) a.sums[(size_t)m * kRemapChunks + blockIdx.x] = s;
 }
 
 }  // namespace
@@ -983,10 +1038,11 @@ hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t 
 }
 
 hipError_t launch_remap(const RemapArgs& a, hipStream_t s) {
-  launch_k(remap_partial_kernel, dim3(kRemapChunks, a.B * 2), 256, 0, s, a);
-  launch_k(remap_finish_kernel, 1, 64, 0, s, a);
-  const int64_t n = (int64_t)a.B * (a.Nv * a.Cv + a.Na * a.A);
-  launch_k(remap_apply_kernel, (unsigned)((n + 255) / 256), 256, 0, s, a);
+  const int nch = std::max(reduce_chunks((int64_t)a.Nv * a.Cv), reduce_chunks((int64_t)a.Na * a.A));
+  launch_k(remap_partial_kernel, dim3(nch, a.B * 2), 256, 0, s, a);
+  launch_k(remap_finish_kernel, a.B * 2, 256, 0, s, a);
+  const int64_t traj = (int64_t)a.Nv * a.Cv + (int64_t)a.Na * a.A;
+  launch_k(remap_apply_kernel, dim3((unsigned)((traj + 255) / 256), a.B), 256, 0, s, a);
   return hipGetLastError();
 }
 
@@ -1001,7 +1057,9 @@ hipError_t launch_or_sums(int n_comp, const float* const* u_hat, const float* co
     a.inv_delta[m] = 1.0 / delta[m];
   }
   a.sums = sums;
-  launch_k(or_sums_kernel, n_comp, 256, 0, s, a);
+  int nch = 1;
+  for (int m = 0; m < n_comp; ++m) nch = std::max(nch, reduce_chunks(n[m]));
+  launch_k(or_sums_kernel, dim3(nch, n_comp), 256, 0, s, a);
   return hipGetLastError();
 }
 
@@ -1017,7 +1075,7 @@ hipError_t launch_or_sums(int n_comp, const float* const* u_hat, const float* co
 namespace wam {
 namespace {
 
-constexpr int kNoAllocScratchDoubles = WAM_MAX_BATCH * 2 * (1 + kRemapChunks);  // 16.6 KB
+constexpr int kNoAllocScratchDoubles = WAM_MAX_BATCH * 2 * (1 + kRemapChunks);  // 256.3 KiB
 constexpr int kMaxDevices = 64;
 
 __device__ __align__(256) double scratch[kNoAllocScratchDoubles];
@@ -1060,7 +1118,7 @@ int wam_remap_noalloc(const wam_config* cfg, const wam_remap_args* a, void* hip_
   if (!cfg || !a) return noalloc_fail(WAM_E_ARG, "wam_remap_noalloc: null argument");
   if (cfg->B < 1 || cfg->B > WAM_MAX_BATCH)
     return noalloc_fail(WAM_E_SHAPE, "wam_remap_noalloc: batch must be 1..WAM_MAX_BATCH (16): the static "
-                                     "scratch holds 16 x 2 x 65 float64 sums");
+                                     "scratch holds 16 x 2 x 1025 float64 sums");
   if (cfg->Nv < 0 || cfg->Na < 0 || cfg->Cv < 1 || cfg->A < 1 || cfg->Nv + cfg->Na < 1)
     return noalloc_fail(WAM_E_SHAPE, "wam_remap_noalloc: need Nv, Na >= 0, Nv + Na >= 1, Cv, A >= 1");
   const int64_t traj = (int64_t)cfg->Nv * cfg->Cv + (int64_t)cfg->Na * cfg->A;

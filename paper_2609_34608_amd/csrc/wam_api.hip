@@ -194,7 +194,7 @@ WsLayout ws_layout(const Dims& d) {
   w.rr_rows = take((size_t)d.M * 3 * 8);
   w.rr_res = take((size_t)d.B * 2 * 8 * 8);
   w.tr_rms = take((size_t)d.B * 2 * (1 + kRemapChunks) * 8);  // rms, then the run sums
-  w.or_sums = take(WAM_MAX_COMPONENTS * 8);
+  w.or_sums = take((size_t)WAM_MAX_COMPONENTS * kRemapChunks * 8);  // run sums per component
   size_t split = 0;
   if (d.bf) {
     split = std::max(split, gemm_partial_floats(d.M, 3 * d.D, d.D, EPI_QKV));
@@ -243,7 +243,7 @@ struct wam_handle {
   // the condition the retained denoising state continues under (cond_buf):
   // set by WAM_ADAPT_REBIND and by every replan (its real condition)
   bool cond_bound = false;
-  double* host_stage = nullptr;  // pinned, small
+  double* host_stage = nullptr;  // pinned, 64 KiB
   std::string err;
   ProfSlot prof[WAM_KC_COUNT];
   // per-layer fixed softmax reference (log2 units) of the bf16 attention, or
@@ -819,7 +819,10 @@ int wam_init(const wam_config* cfg, const float* hw, size_t n_hw, void* dev_weig
   h->wdev = static_cast<char*>(dev_weights);
   h->wsdev = static_cast<char*>(dev_ws);
   h->stream = static_cast<hipStream_t>(stream);
-  if (hipHostMalloc((void**)&h->host_stage, 4096, hipHostMallocDefault) != hipSuccess) {
+  // gate statistics (B x 2 x 8 doubles) or the score's run sums (components x runs)
+  constexpr size_t kStageBytes = (size_t)WAM_MAX_COMPONENTS * kRemapChunks * 8;
+  static_assert(kStageBytes >= (size_t)WAM_MAX_BATCH * 2 * 8 * 8, "host staging size");
+  if (hipHostMalloc((void**)&h->host_stage, kStageBytes, hipHostMallocDefault) != hipSuccess) {
     delete h;
     return WAM_E_HIP;
   }
@@ -1083,11 +1086,14 @@ int wam_consistency_score(wam_t h, int n, const float* const* u_hat, const float
   if (!(wsum > 0.0)) return fail(h, WAM_E_ARG, "weights sum to zero");
   double* sums = h->S<double>(h->ws.or_sums);
   HIPCHK(h, launch_or_sums(n, u_hat, u, cnt, delta, sums, h->stream));
-  HIPCHK(h, hipMemcpyAsync(h->host_stage, sums, n * 8, hipMemcpyDeviceToHost, h->stream));
+  HIPCHK(h, hipMemcpyAsync(h->host_stage, sums, (size_t)n * kRemapChunks * 8, hipMemcpyDeviceToHost, h->stream));
   HIPCHK(h, hipStreamSynchronize(h->stream));
   double acc = 0.0;
   for (int m = 0; m < n; ++m) {
-    const double e2 = h->host_stage[m] / (double)cnt[m];  // e_m^2
+    double sm = 0.0;  // the component's run sums, in run order
+    const double* runs = h->host_stage + (size_t)m * kRemapChunks;
+    for (int c = 0; c < reduce_chunks(cnt[m]); ++c) sm += runs[c];
+    const double e2 = sm / (double)cnt[m];  // e_m^2
     acc += weight[m] * e2;
   }
   *S_out = sqrt(acc / wsum);

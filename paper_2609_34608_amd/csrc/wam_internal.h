@@ -265,10 +265,19 @@ hipError_t launch_pack_condition(const float* obs, int n_obs, int c_obs, const f
 hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t s);
 
 // Trajectory Remapping
-constexpr int kRemapChunks = 64;  // runs per (sample, branch) of the remap rms sums
+// Chunked float64 reductions (remap rms, rebinding score): a reduction over n
+// elements is cut into reduce_chunks(n) runs of equal length (at least
+// kReduceRun elements each, at most kRemapChunks runs), one block per run,
+// and the run sums are added in run order.
+constexpr int kRemapChunks = 1024;
+constexpr int kReduceRun = 2048;
+__host__ __device__ inline int reduce_chunks(int64_t n) {
+  const int64_t c = (n + kReduceRun - 1) / kReduceRun;
+  return (int)(c < 1 ? 1 : (c > kRemapChunks ? kRemapChunks : c));
+}
 struct RemapArgs {
   const float* x_bar; const float* x_r; const float* noise; float* x_out;
-  double* rms;      // [B][2] scratch
+  double* coef;     // [B][2] scratch: sigma_b0 / (sigma_r rms) per (sample, branch)
   double* partial;  // [B][2][kRemapChunks] scratch
   float sigma_r, sigma_b0;
   int shift_action, shift_video;
@@ -277,6 +286,7 @@ struct RemapArgs {
 hipError_t launch_remap(const RemapArgs& a, hipStream_t s);
 
 // Observation Rebinding: sums of ((u_hat-u)/delta)^2 per component, float64
+// run sums [n_comp][kRemapChunks] (the first reduce_chunks(n[m]) of row m)
 hipError_t launch_or_sums(int n_comp, const float* const* u_hat, const float* const* u,
                           const int64_t* n, const double* delta, double* sums, hipStream_t s);
 
