@@ -8,6 +8,8 @@
 #include <string>
 #include <vector>
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include "wam_internal.h"
 
 using namespace wam;
@@ -289,6 +291,15 @@ int fail(wam_t h, int code, const std::string& msg) {
   } while (0)
 
 float* mod_table(wam_t h) { return h->S(h->ws.mod) + (size_t)h->mod_k * h->d.Nmod; }
+
+// roctx range over one phase of a replan or one denoising step (host-side
+// annotations for a marker trace; they cost nothing without a profiler).
+struct Phase {
+  explicit Phase(const char* name) { roctxRangePushA(name); }
+  ~Phase() { roctxRangePop(); }
+  Phase(const Phase&) = delete;
+  Phase& operator=(const Phase&) = delete;
+};
 
 // ---- per-launch timing for the measurement API
 struct ProfScope {
@@ -741,7 +752,11 @@ int continue_impl(wam_t h, int k_from, int k_to, float* x, const float* cond, co
       int st = copy_traj(h, x_capture, x);
       if (st) return st;
     }
-    int st = forward(h, k, x, cond, nullptr, x, rr, infos ? &infos[k - k_from] : nullptr);
+    int st;
+    {
+      Phase ph("wam: denoising step");
+      st = forward(h, k, x, cond, nullptr, x, rr, infos ? &infos[k - k_from] : nullptr);
+    }
     if (st) return st;
   }
   if (capture_stage == k_to && x_capture) {
@@ -1183,6 +1198,7 @@ int wam_replan_begin(wam_t h, const wam_replan_args* a) {
   }
   const Dims& d = h->d;
   float* x_init = h->S(h->ws.x_init);
+  Phase ph_begin("wam_replan_begin: remap + anticipatory prefix");
   if (a->tr_enabled) {
     RemapArgs r{h->S(h->ws.x_bar), h->S(h->ws.x_r), a->noise_remap, x_init, h->S<double>(h->ws.tr_rms),
                 h->S<double>(h->ws.tr_rms) + 2 * d.B,
@@ -1212,6 +1228,7 @@ int wam_replan_end(wam_t h, const wam_replan_args* a, wam_replan_info* info) {
   float* xw = h->S(h->ws.x_work);
   wam_replan_info* inf = &p.info;
   if (p.first) {
+    Phase ph("wam_replan_end: first replan (native)");
     if ((st = copy_traj(h, xw, a->noise_first))) return st;
     if ((st = run_segment(h, a, 0, K, a->cond_real, a->rr_first, true))) return st;
     inf->path = WAM_PATH_FIRST;
@@ -1219,25 +1236,31 @@ int wam_replan_end(wam_t h, const wam_replan_args* a, wam_replan_info* info) {
     const wam_rr_profile* rrp = (a->rr_prefix && a->rr.mode != WAM_RR_OFF) ? &a->rr : nullptr;
     if ((st = read_history(h, p.entry, p.entry + a->k1, rrp, p.steps))) return st;
     double S = 0.0;
-    st = wam_consistency_score(h, a->n_components, a->u_hat, a->u, a->n, a->delta, a->weight, &S);
+    {
+      Phase ph("wam_replan_end: consistency score");
+      st = wam_consistency_score(h, a->n_components, a->u_hat, a->u, a->n, a->delta, a->weight, &S);
+    }
     if (st) return st;
     inf->S = S;
     if (S < a->tau && h->kappa < a->kappa_max) {
       h->kappa += 1;
       inf->n_bind = 1;
       inf->path = WAM_PATH_ACCEPT;
+      Phase ph("wam_replan_end: rebind + continuation");
       if ((st = bind_condition(h, a->cond_real))) return st;
       if ((st = run_segment(h, a, p.entry + a->k1, K, resolve_cond(h, nullptr), a->rr_prefix, true)))
         return st;
     } else {
       h->kappa = 0;
       inf->path = WAM_PATH_REJECT;
+      Phase ph("wam_replan_end: restart from the remapped initialisation");
       h->layer_valid = false;
       if ((st = copy_traj(h, xw, h->S(h->ws.x_init)))) return st;
       if ((st = run_segment(h, a, p.entry, K, a->cond_real, a->rr_refresh, true))) return st;
     }
   } else {
     inf->path = a->or_enabled ? WAM_PATH_FORCED : WAM_PATH_DIRECT;
+    Phase ph("wam_replan_end: refresh under the real condition");
     if (a->or_enabled) h->kappa = 0;
     if ((st = run_segment(h, a, p.entry, K, a->cond_real, a->rr_refresh, true))) return st;
   }
