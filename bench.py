@@ -345,6 +345,11 @@ def sweep(args):
     print(json.dumps({"sweep": rows}), flush=True)
 
 
+def progress(msg: str) -> None:
+    """One progress line on stderr (the JSON result stays the only stdout line)."""
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
 def achievable_peaks():
     """What the chip reaches in practice: the bf16 MFMA issue rate on register
     operands (both MFMA shapes) and a streaming copy of 1 GiB."""
@@ -371,7 +376,9 @@ def measure(args, name, steps, warmup, cpu, native, adapt, copy_probe_mib=0):
 
     spec = get_workload(name)
     dev = torch.device("cuda:0")
+    progress(f"{name}: generating weights")
     W = make_weights(spec)
+    progress(f"{name}: weights ready")
     m = R.WamModel(R.config_of(spec), W, device=dev, own_stream=args.exec == "graph")
     m.set_option(L.WAM_OPT_ATTENTION, ATTN_VARIANTS[args.attention])
     if args.exec in ("device", "graph"):
@@ -446,6 +453,7 @@ def measure(args, name, steps, warmup, cpu, native, adapt, copy_probe_mib=0):
     elapsed = time.perf_counter() - t0
     dom_ms, dom_n, dom_work = m.profile_read(dom)
     m.profile_enable(dom, False)
+    progress(f"{name}: timed region done ({steps} replans in {elapsed:.2f} s)")
 
     n_steps = sum(i.steps for i in infos)
     layers_eval = sum(i.steps * spec.L - i.layers_skipped for i in infos)
@@ -527,7 +535,9 @@ def measure(args, name, steps, warmup, cpu, native, adapt, copy_probe_mib=0):
         out["reuse_latency_speedup"] = round(nat / (elapsed / steps), 4)
 
     if cpu:
-        out["cpu_baseline"] = (cpu_baseline_layer(spec, W) if spec.name == "large"
+        progress(f"{name}: float64 oracle on the host")
+        # models whose float64 step would take minutes are timed one layer at a time
+        out["cpu_baseline"] = (cpu_baseline_layer(spec, W) if spec.flops_per_step() > 1e12
                                else cpu_baseline(spec, W, obs, args.cpu_sample_steps))
     m.close()
     return out
