@@ -319,7 +319,13 @@ int wam_hidden(wam_t h, int k, const float *x, const float *cond, int n_layers, 
 int wam_adapt_state(wam_t h, int op, const void *args);
 /* Observation Rebinding score (Eq. bind-discrepancy) over device arrays,
  * accumulated in float64: S = sqrt(sum w e^2 / sum w),
- * e_m = sqrt(mean(((u_hat_m - u_m)/delta_m)^2)).  Synchronises. */
+ * e_m = sqrt(mean(((u_hat_m - u_m)/delta_m)^2)).  u_hat[m], u[m]: device
+ * float[n[m]], caller-owned; n_components in 1..WAM_MAX_COMPONENTS, n >= 1,
+ * delta > 0, weight >= 0 with a positive sum (else WAM_E_ARG).  The squared
+ * differences are summed on the device in runs (float64, fixed order) and the
+ * run sums on the host.  Only this device form exists: the components are the
+ * condition tensors, which already live on the device.  Uses the handle's
+ * stream and workspace; synchronises. */
 int wam_consistency_score(wam_t h, int n_components, const float *const *u_hat,
                           const float *const *u, const int64_t *n, const double *delta,
                           const double *weight, double *S_out);
