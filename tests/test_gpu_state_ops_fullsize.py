@@ -1,0 +1,88 @@
+"""Trajectory Remapping (Sec. 3.1, Eq. direction, transport, app-transport-rms)
+and the rebinding score (Sec. 3.2, Eq. bind-discrepancy) at the workload
+sizes and beyond, through the C ABI, against the oracle.
+
+Both reduce in float64 over runs of the input (at least 2048 elements each,
+at most 1024 runs per sample and branch, or per component) whose sums are
+then added in a fixed order.  The small-shape tests fit in one run; these
+cover many runs (the mid and large trajectories: 16 and 75 runs of the video
+branch), runs longer than the minimum (a 4 M-element video branch: 1024 runs
+of 4096) and ragged ends.  The remap goes through wam_remap_noalloc, which
+needs no weights and runs the same kernels as wam_adapt_state(REMAP); at the
+large shape the handle's REMAP is compared with it bit for bit.
+"""
+import numpy as np
+import pytest
+
+from oracle import method as OM
+from synth import get_workload, make_weights
+from gpu_common import device, to_dev, rel_err
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return device()
+
+
+def _remap_case(dev, spec, seed, shift_a, shift_v):
+    from paper_2609_34608_amd import runtime as R
+    rng = np.random.default_rng(seed)
+    xb, xr, eps = (rng.standard_normal((spec.B, spec.traj)).astype(np.float32) for _ in range(3))
+    sr, sb = np.float32(0.55), np.float32(0.5)
+    args = [to_dev(xb, dev), to_dev(xr, dev), float(sr), float(sb), shift_a, shift_v, to_dev(eps, dev)]
+    out = to_dev(np.full((spec.B, spec.traj), np.nan, np.float32), dev)
+    R.remap_noalloc(R.config_of(spec), *args, out)
+    got = out.cpu().numpy()
+    d = OM.tr_direction(spec, xr, xb, float(sr))
+    ref = OM.tr_remap(spec, xb, d, float(sb), shift_a, shift_v, eps)
+    err = rel_err(got, ref)
+    print(f"remap B{spec.B} traj {spec.traj} shifts ({shift_a}, {shift_v}): rel err {err:.2e}")
+    assert err <= 1e-6
+    return args, got
+
+
+@pytest.mark.parametrize("name,shift_a,shift_v", [("mid", 8, 0), ("mid", 0, 0), ("large", 8, 0), ("large", 3, 2)])
+def test_remap_at_workload_size(dev, name, shift_a, shift_v):
+    _remap_case(dev, get_workload(name), 31, shift_a, shift_v)
+
+
+def test_remap_long_runs(dev):
+    """A 4 M-element video branch per sample (runs of 4096), two samples."""
+    spec = get_workload("tiny").replace(B=2, Nv=262144, Na=40)
+    _remap_case(dev, spec, 32, 5, 1)
+
+
+def test_handle_remap_equals_noalloc_at_large_size(dev):
+    from paper_2609_34608_amd import runtime as R
+    spec = get_workload("large")
+    # the remap reads only the trajectory dimensions: a handle with the large
+    # trajectory and a two-layer float32 DiT
+    lite = spec.replace(L=2, D=128, H=4, F=512, dtype="fp32")
+    m = R.WamModel(R.config_of(lite), make_weights(lite), device=dev)
+    try:
+        args, got = _remap_case(dev, spec, 33, 8, 0)
+        ref_dev = m.remap(*args)
+        np.testing.assert_array_equal(got, ref_dev.cpu().numpy())
+    finally:
+        m.close()
+
+
+def test_consistency_score_many_runs(dev):
+    """Components of 3 M, 4 M + 3 (ragged) and 5000 elements."""
+    from paper_2609_34608_amd import runtime as R
+    spec = get_workload("tiny")
+    m = R.WamModel(R.config_of(spec), make_weights(spec), device=dev)
+    try:
+        rng = np.random.default_rng(34)
+        comps = [(rng.standard_normal(n).astype(np.float32), rng.standard_normal(n).astype(np.float32))
+                 for n in (3_000_000, 4 * 2 ** 20 + 3, 5000)]
+        delta, weight = [2.0, 0.25, 16.0], [0.2, 0.5, 0.3]
+        S = m.consistency_score([to_dev(a, dev) for a, _ in comps], [to_dev(b, dev) for _, b in comps],
+                                delta, weight)
+        ref = OM.or_score([OM.or_component_error(a, b, dl) for (a, b), dl in zip(comps, delta)], weight)
+        print(f"score {S!r} oracle {ref!r}")
+        assert S == pytest.approx(ref, rel=1e-12)
+    finally:
+        m.close()
