@@ -354,14 +354,19 @@ def achievable_peaks():
     """What the chip reaches in practice: the bf16 MFMA issue rate on register
     operands (both MFMA shapes) and a streaming copy of 1 GiB."""
     from paper_2609_34608_amd import runtime as R
-    t16, _ = R.probe_mfma_bf16(shape=0)
-    t32, _ = R.probe_mfma_bf16(shape=1)
-    gbs, _ = R.probe_copy(1 << 30, reps=5)
+    # each timed launch lasts ~90 ms after a warm-up launch of the same length:
+    # launches of a few ms end before the shader clock has ramped up from idle
+    # and read ~20% low
+    iters = 400_000
+    t16, _ = R.probe_mfma_bf16(shape=0, iters=iters)
+    t32, _ = R.probe_mfma_bf16(shape=1, iters=iters)
+    gbs, _ = R.probe_copy(1 << 30, reps=100)
     return {"mfma_bf16_16x16x32_tflops": round(t16, 1), "mfma_bf16_32x32x16_tflops": round(t32, 1),
             "copy_gbs": round(gbs, 1),
-            "method": "wam_probe_mfma_bf16 (1024 blocks x 4 waves, 20000 rounds of independent MFMA chains "
-                      "on register operands) and wam_probe_copy (1 GiB device copy, one 16-byte element per thread, read + "
-                      "write bytes counted), HIP events"}
+            "method": f"wam_probe_mfma_bf16 (1024 blocks x 4 waves, {iters} rounds of independent MFMA chains "
+                      "on register operands, one timed launch after a warm-up launch) and wam_probe_copy "
+                      "(1 GiB device copy, one 16-byte element per thread, read + write bytes counted, 100 "
+                      "timed copies), HIP events"}
 
 
 def measure(args, name, steps, warmup, cpu, native, adapt, copy_probe_mib=0):

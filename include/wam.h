@@ -404,7 +404,9 @@ int wam_profile_read(wam_t h, int kc, double *total_ms, int64_t *launches, doubl
  * kernels; shape 1: v_mfma_f32_32x32x16_bf16), 131072 FLOP per wave per
  * round, after one untimed warm-up launch.  sink: device float[n_blocks *
  * 256], caller-owned, receives one value per thread.  Outputs the rate in
- * TFLOP/s and the timed launch in ms.
+ * TFLOP/s and the timed launch in ms.  Size iters so that a launch lasts
+ * tens of ms or more: the shader clock ramps up from idle over that time,
+ * and launches of a few ms read up to ~20% low.
  *
  * wam_probe_copy: copies bytes (a multiple of 16, both pointers 16-byte
  * aligned, device, caller-owned, not overlapping) from src to dst reps times
