@@ -498,6 +498,10 @@ def measure(args, name, steps, warmup, cpu, native, adapt, copy_probe_mib=0):
         },
         "action_chunks_per_s": round(chunks_per_s, 3),
         "denoise_steps_per_replan": n_steps / steps,
+        # a batched step denoises B samples (and a replan yields B chunks)
+        "batch": spec.B,
+        "sample_steps_per_s": round(steps_per_s * spec.B, 3),
+        "sample_chunks_per_s": round(chunks_per_s * spec.B, 3),
         "mfma_frac_dit": round(flops / elapsed / 1e12 / MFMA_BF16_PEAK_TFLOPS, 5),
         "dit_tflops": round(flops / elapsed / 1e12, 3),
         "reuse_stats": {"rr_accept": n_reuse / n_att if n_att else None,
