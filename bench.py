@@ -206,6 +206,9 @@ def parse():
     p.add_argument("--no-replay", action="store_true",
                    help="skip the extra small-model closed-loop replay figures")
     p.add_argument("--cpu-sample-steps", type=int, default=5)
+    p.add_argument("--tau", type=float, default=None,
+                   help="Observation Rebinding threshold tau (default: the workload's, 0.5; 0.3 rejects every "
+                        "rebinding on the AR(1) observations, whose score is ~0.44)")
     p.add_argument("--rr-mode", default="auto", choices=["auto", "force_skip", "force_full", "off"],
                    help="residual-rescaling mode of the timed replans")
     p.add_argument("--exec", default="host", choices=["host", "device", "graph"],
@@ -380,6 +383,8 @@ def measure(args, name, steps, warmup, cpu, native, adapt, copy_probe_mib=0):
     from synth import get_workload, make_weights, make_initial_noise, make_observations, make_remap_noise
 
     spec = get_workload(name)
+    if args.tau is not None:
+        spec = spec.replace(or_tau=args.tau)
     dev = torch.device("cuda:0")
     progress(f"{name}: generating weights")
     W = make_weights(spec)
@@ -491,7 +496,7 @@ def measure(args, name, steps, warmup, cpu, native, adapt, copy_probe_mib=0):
             "workload": (f"{spec.name}: closed-loop replan with TR+OR+RR on a joint video/action DiT "
                          f"B{spec.B} L{spec.L} D{spec.D} H{spec.H} F{spec.F} T{spec.T} "
                          f"(video {spec.Nv}, action {spec.Na}x{spec.A}, obs {spec.No}) K{spec.K} "
-                         f"b0={spec.tr_b0} k1={spec.or_k1} shift={spec.shift_action}"),
+                         f"b0={spec.tr_b0} k1={spec.or_k1} tau={spec.or_tau} shift={spec.shift_action}"),
             "step": "one replan (control step)",
             "exec": args.exec,
             "attention": args.attention,
