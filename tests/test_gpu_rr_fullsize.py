@@ -111,3 +111,31 @@ def test_full_size_rr_gate_and_injection(dev, name):
             assert moved >= 10 * BF16_TOL, moved
     finally:
         OD.ATTENTION_THREADS = threads
+
+
+@pytest.mark.parametrize("name", ["small", "mid", "large"])
+def test_bf16_steps_with_rr_are_deterministic(dev, name):
+    """Four denoising steps with Residual Rescaling forced on (the first
+    establishes the layer state, the next three inject), run twice from the
+    same state: the trajectory and every reported statistic are the same bits
+    (the GEMM, attention and reduction kernels sum in fixed orders, with no
+    atomics), which the decision-trace protocol relies on."""
+    from paper_2609_34608_amd import _lib as L
+    spec, W, m = model_for(name, dev)
+    sig = f32_sigmas(spec.K)
+    m.set_schedule(sig)
+    skip_g, _ = rr_of(spec, L.WAM_RR_FORCE_SKIP)
+    cd = to_dev(make_observations(spec, 0)[0], dev)
+    x0 = to_dev(make_initial_noise(spec), dev)
+    runs = []
+    for _ in range(2):
+        m.reset_layer_state()
+        x = x0.clone()
+        infos = m.continue_(0, 4, x, cd, rr=skip_g)
+        runs.append((x.cpu().numpy(), infos))
+    np.testing.assert_array_equal(runs[0][0], runs[1][0])
+    for a, b in zip(runs[0][1], runs[1][1]):
+        assert (a.attempted, a.accepted) == (b.attempted, b.accepted)
+        for f in ("alpha", "cos", "fit"):
+            np.testing.assert_array_equal(getattr(a, f), getattr(b, f))
+    assert sum(i.accepted for i in runs[0][1]) == 3
