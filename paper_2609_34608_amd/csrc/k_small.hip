@@ -142,42 +142,65 @@ __global__ void embed_kernel(EmbedArgs a) {
   }
 }
 
-// Vectorised form: one block per token row, thread i owns columns 4i..4i+3
-// (D / 4 threads), and every load it needs (bias, position embedding and the
-// up to kEmbedC weight rows, clamped to the branch's channel count against
-// zero-padded token values) is issued before the sums: one round trip where
-// the loop over a run-time channel count waited on each batch of weights.
+// Vectorised form: a block takes up to R consecutive rows of one branch
+// (video, action or observation tokens) of one sample, so that the branch's
+// weight rows are read once for all of them (with one row per block the
+// weight reads from L2 outweighed the HBM traffic of long sequences: 66 ->
+// 33 us at T = 10176 with R = 8); thread i owns columns 4i..4i+3 (D / 4
+// threads).  Every load a thread needs (bias, the up to kEmbedC weight rows,
+// clamped to the branch's channel count against zero-padded token values,
+// and the position-embedding rows) is issued before the sums.
 constexpr int kEmbedC = 16;
+__host__ __device__ inline int embed_blocks_per_sample(int Nv, int Na, int No, int R) {
+  return (Nv + R - 1) / R + (Na + R - 1) / R + (No + R - 1) / R;
+}
+template <int R>
 __global__ __launch_bounds__(512) void embed_v4_kernel(EmbedArgs a) {
-  const int row = blockIdx.x;  // b*T + t
-  const int b = row / a.T, t = row % a.T;
-  __shared__ float tok[kEmbedC];
+  constexpr int kEmbedRows = R;
+  const int per = embed_blocks_per_sample(a.Nv, a.Na, a.No, R);
+  const int b = blockIdx.x / per, j = blockIdx.x % per;
+  const int gv = (a.Nv + kEmbedRows - 1) / kEmbedRows, ga = (a.Na + kEmbedRows - 1) / kEmbedRows;
   const float* w;
   const float* bias;
-  const float* src;
-  int c;
+  const float* src;  // token values of the block's first row
+  int c, t0, n;      // channels, first row (within the sample), rows of this block
   const int traj = a.Nv * a.Cv + a.Na * a.A;
-  if (t < a.Nv) {
-    c = a.Cv, w = a.wv, bias = a.bv, src = a.x + (size_t)b * traj + (size_t)t * a.Cv;
-  } else if (t < a.Nv + a.Na) {
-    c = a.A, w = a.wa, bias = a.ba, src = a.x + (size_t)b * traj + (size_t)a.Nv * a.Cv + (size_t)(t - a.Nv) * a.A;
+  if (j < gv) {
+    t0 = j * kEmbedRows, n = min(kEmbedRows, a.Nv - t0), c = a.Cv, w = a.wv, bias = a.bv;
+    src = a.x + (size_t)b * traj + (size_t)t0 * a.Cv;
+  } else if (j < gv + ga) {
+    const int i0 = (j - gv) * kEmbedRows;
+    t0 = a.Nv + i0, n = min(kEmbedRows, a.Na - i0), c = a.A, w = a.wa, bias = a.ba;
+    src = a.x + (size_t)b * traj + (size_t)a.Nv * a.Cv + (size_t)i0 * a.A;
   } else {
-    c = a.Co, w = a.wo, bias = a.bo, src = a.cond + ((size_t)b * a.No + (t - a.Nv - a.Na)) * a.Co;
+    const int i0 = (j - gv - ga) * kEmbedRows;
+    t0 = a.Nv + a.Na + i0, n = min(kEmbedRows, a.No - i0), c = a.Co, w = a.wo, bias = a.bo;
+    src = a.cond + ((size_t)b * a.No + i0) * a.Co;
   }
-  if (threadIdx.x < kEmbedC) tok[threadIdx.x] = threadIdx.x < c ? src[threadIdx.x] : 0.f;
+  __shared__ float tok[kEmbedRows][kEmbedC];
+  for (int i = threadIdx.x; i < kEmbedRows * kEmbedC; i += blockDim.x) {
+    const int r = i / kEmbedC, ch = i % kEmbedC;
+    tok[r][ch] = r < n && ch < c ? src[(size_t)r * c + ch] : 0.f;
+  }
   const int col = threadIdx.x * 4;
   const bool live = col < a.D;
   const int cc = live ? col : 0;
   const f32x4 b4 = *reinterpret_cast<const f32x4*>(bias + cc);
-  const f32x4 p4 = *reinterpret_cast<const f32x4*>(a.pe + (size_t)t * a.D + cc);
-  f32x4 w4[kEmbedC];
+  f32x4 w4[kEmbedC], p4[kEmbedRows];
 #pragma unroll
-  for (int j = 0; j < kEmbedC; ++j) w4[j] = *reinterpret_cast<const f32x4*>(w + (size_t)min(j, c - 1) * a.D + cc);
+  for (int k = 0; k < kEmbedC; ++k) w4[k] = *reinterpret_cast<const f32x4*>(w + (size_t)min(k, c - 1) * a.D + cc);
+#pragma unroll
+  for (int r = 0; r < kEmbedRows; ++r)
+    p4[r] = *reinterpret_cast<const f32x4*>(a.pe + (size_t)(t0 + min(r, n - 1)) * a.D + cc);
   __syncthreads();
-  f32x4 acc = b4;
 #pragma unroll
-  for (int j = 0; j < kEmbedC; ++j) acc += tok[j] * w4[j];
-  if (live) *reinterpret_cast<f32x4*>(a.h + (size_t)row * a.D + col) = acc + p4;
+  for (int r = 0; r < kEmbedRows; ++r) {
+    if (r >= n) break;
+    f32x4 acc = b4;
+#pragma unroll
+    for (int k = 0; k < kEmbedC; ++k) acc += tok[r][k] * w4[k];
+    if (live) *reinterpret_cast<f32x4*>(a.h + ((size_t)b * a.T + t0 + r) * a.D + col) = acc + p4[r];
+  }
 }
 
 // ------------------------------------------------------------- LN + modulation
@@ -915,7 +938,17 @@ hipError_t launch_embed(const EmbedArgs& a, hipStream_t s) {
   const bool chans = (a.Nv == 0 || a.Cv >= 1) && (a.Na == 0 || a.A >= 1) && (a.No == 0 || a.Co >= 1);
   if (a.D % 4 == 0 && a.D <= 2048 && a.Cv <= kEmbedC && a.A <= kEmbedC && a.Co <= kEmbedC && chans) {
     const int threads = (a.D / 4 + kWave - 1) / kWave * kWave;
-    launch_k(embed_v4_kernel, a.B * a.T, threads, 0, s, a);
+    // rows per block: share the weight reads where the grid stays above
+    // ~1000 blocks, one row per block for short sequences (latency)
+    const long rows = (long)a.B * a.T;
+    if (rows >= 8192)
+      launch_k(embed_v4_kernel<8>, a.B * embed_blocks_per_sample(a.Nv, a.Na, a.No, 8), threads, 0, s, a);
+    else if (rows >= 4096)
+      launch_k(embed_v4_kernel<4>, a.B * embed_blocks_per_sample(a.Nv, a.Na, a.No, 4), threads, 0, s, a);
+    else if (rows >= 2048)
+      launch_k(embed_v4_kernel<2>, a.B * embed_blocks_per_sample(a.Nv, a.Na, a.No, 2), threads, 0, s, a);
+    else
+      launch_k(embed_v4_kernel<1>, a.B * embed_blocks_per_sample(a.Nv, a.Na, a.No, 1), threads, 0, s, a);
   } else {
     launch_k(embed_kernel, a.B * a.T, 256, 0, s, a);
   }
@@ -955,8 +988,13 @@ hipError_t launch_final(const FinalArgs& a, hipStream_t s) {
   if (a.D % kWave || a.D / kWave > kMaxVpl || a.Cv > kFinalCout || a.A > kFinalCout) return hipErrorInvalidValue;
   // widest column vector D allows; rows per wave within the register budget
   if (a.D % (4 * kWave) == 0) {
-    if (a.D <= 1536)
+    // four rows per wave share each head-weight chunk; short trajectories
+    // (under 4096 rows: 200 waves of four rows on the small model) take one
+    // row per wave instead, so that enough waves hide the memory latency
+    if (a.D <= 1536 && (long)a.B * (a.Nv + a.Na) >= 4096)
       launch_final_t<4, 4, 6>(a, s);
+    else if (a.D <= 1536)
+      launch_final_t<4, 1, 6>(a, s);
     else
       launch_final_t<4, 2, 8>(a, s);
   } else if (a.D % (2 * kWave) == 0 && a.D <= 1024) {
