@@ -456,8 +456,12 @@ def measure(args, name, steps, warmup, cpu, native, adapt, copy_probe_mib=0):
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     infos = []
+    per_replan = []  # wall time of each replan, chunk ready (a control step waits for it)
     for _ in range(steps):
+        ts = time.perf_counter()
         infos.append(replan(t))
+        torch.cuda.synchronize()
+        per_replan.append(time.perf_counter() - ts)
         t += 1
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
@@ -503,6 +507,8 @@ def measure(args, name, steps, warmup, cpu, native, adapt, copy_probe_mib=0):
         },
         "action_chunks_per_s": round(chunks_per_s, 3),
         "denoise_steps_per_replan": n_steps / steps,
+        "ms_per_replan_median": round(1000.0 * float(np.median(per_replan)), 4),
+        "ms_per_replan_min_max": [round(1000.0 * min(per_replan), 4), round(1000.0 * max(per_replan), 4)],
         # a batched step denoises B samples (and a replan yields B chunks)
         "batch": spec.B,
         "sample_steps_per_s": round(steps_per_s * spec.B, 3),
