@@ -10,6 +10,8 @@
     (Sec. 3.3, Eq. residual-injection): the change that injection makes to
     the velocity (reuse minus full computation on the same input) against the
     oracle's under the same forced decision, and alpha per branch.
+  * The host-decision, device-decision and graph-replay ways of running a
+    replan give the same bits at the small bf16 model's shape.
 """
 from collections import deque
 
@@ -233,3 +235,58 @@ def test_free_running_decision_agreement(dev, name):
     assert n_att >= 3
     for k, margin in flips:
         assert margin <= 1e-2, (k, margin)
+
+
+@pytest.mark.parametrize("rr_mode", ["AUTO", "FORCE_SKIP"])
+def test_exec_modes_agree_at_small_bf16(dev, rr_mode):
+    """The three ways of running a replan at the small bf16 model's shape
+    (closed-loop replay: TR + OR + RR, action shift 8) give the same bits:
+    host decision (the gate read back per step), device decision (a flag
+    kernel predicates the inject or middle / refresh launches) and captured
+    step graphs replayed with the device decision.  Five replans cover the
+    first, accepted and forced-refresh paths; with reuse forced the predicated
+    inject runs, with AUTO (every gate fails on these weights) the middle."""
+    from paper_2609_34608_amd import _lib as L
+    spec0 = model_for("replay", dev)[0]
+    rr_g, _ = rr_of(spec0, getattr(L, f"WAM_RR_{rr_mode}"))
+    ra = dict(b0=spec0.tr_b0, r=spec0.tr_r, shift_action=spec0.shift_action, shift_video=spec0.shift_video,
+              k1=spec0.or_k1, tau=spec0.or_tau, kappa_max=spec0.or_kappa_max)
+    rho = spec0.ar_rho
+    delta = 1.0 / np.sqrt(1 - rho * rho)
+    n_ctrl = 5
+    obs = make_observations(spec0, n_ctrl)
+
+    def run(own_stream, devdec, graphs):
+        spec, W, m = model_for("replay", dev, own_stream=own_stream)
+        m.set_schedule(f32_sigmas(spec.K))
+        m.set_option(L.WAM_OPT_DEVICE_DECISION, devdec)
+        m.set_option(L.WAM_OPT_GRAPHS, graphs)
+        m.reset_all()
+        x_out = m.new_traj()
+        outs, paths, decisions = [], [], []
+        try:
+            for t in range(n_ctrl):
+                cr = to_dev(obs[t], dev)
+                cp = to_dev((rho * obs[t - 1]).astype(np.float32) if t > 0 else obs[t], dev)
+                info = m.replan(cr, x_out, to_dev(make_remap_noise(spec, t), dev), cond_pred=cp, u_hat=[cp],
+                                u=[cr], delta=[delta], weight=[1.0],
+                                noise_first=to_dev(make_initial_noise(spec), dev), rr=rr_g, **ra)
+                outs.append(x_out.cpu().numpy())
+                paths.append(info.path)
+                decisions.append(list(info.decision[:info.steps]))
+        finally:
+            m.set_option(L.WAM_OPT_GRAPHS, 0)
+            m.set_option(L.WAM_OPT_DEVICE_DECISION, 0)
+        return outs, paths, decisions
+
+    host = run(False, 0, 0)
+    devd = run(False, 1, 0)
+    graph = run(True, 1, 1)
+    assert host[1] == [L.WAM_PATH_FIRST, L.WAM_PATH_ACCEPT, L.WAM_PATH_ACCEPT, L.WAM_PATH_ACCEPT,
+                       L.WAM_PATH_FORCED]
+    if rr_mode == "FORCE_SKIP":
+        assert any(d == 1 for ds in host[2] for d in ds)
+    for other in (devd, graph):
+        assert other[1] == host[1] and other[2] == host[2]
+        for a, b in zip(host[0], other[0]):
+            np.testing.assert_array_equal(a, b)
