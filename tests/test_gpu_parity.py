@@ -109,11 +109,14 @@ def test_determinism(dev):
 _RR_MODELS = ["tiny_rr", "tiny_rr256"]
 
 
-@pytest.mark.parametrize("model", _RR_MODELS)
+@pytest.mark.parametrize("model,B", [(m, 2) for m in _RR_MODELS] + [("tiny_rr256", 16)])
 @pytest.mark.parametrize("mode_name", ["AUTO", "FORCE_SKIP", "FORCE_FULL", "NEVER"])
-def test_rr_modes_match_oracle(dev, mode_name, model):
+def test_rr_modes_match_oracle(dev, mode_name, model, B):
+    """Every RR mode against the oracle forced to the device's decision trace,
+    with alpha / cos / fit per (sample, branch); B = 16 fills the per-sample
+    statistics the ABI reports (WAM_MAX_BATCH)."""
     from paper_2609_34608_amd import _lib as L
-    spec, W, m, sig = _tiny(dev, model, B=2)
+    spec, W, m, sig = _tiny(dev, model, B=B)
     modes = {"AUTO": (L.WAM_RR_AUTO, {}), "FORCE_SKIP": (L.WAM_RR_FORCE_SKIP, {}),
              "FORCE_FULL": (L.WAM_RR_FORCE_FULL, {}), "NEVER": (L.WAM_RR_AUTO, {"gamma_cos": 1.5})}
     mode, kw = modes[mode_name]
