@@ -86,3 +86,26 @@ def test_consistency_score_many_runs(dev):
         assert S == pytest.approx(ref, rel=1e-12)
     finally:
         m.close()
+
+
+def test_consistency_score_max_components(dev):
+    """The most components the ABI takes (WAM_MAX_COMPONENTS = 8), with
+    lengths around the run size (2047, 2048, 2049), a single element, and a
+    4 M + 1 component whose runs are longer than the minimum."""
+    from paper_2609_34608_amd import runtime as R, _lib as L
+    spec = get_workload("tiny")
+    m = R.WamModel(R.config_of(spec), make_weights(spec), device=dev)
+    try:
+        rng = np.random.default_rng(35)
+        sizes = (1, 2047, 2048, 2049, 100_000, 3, 4 * 2 ** 20 + 1, 7)
+        assert len(sizes) == L.WAM_MAX_COMPONENTS
+        comps = [(rng.standard_normal(n).astype(np.float32), rng.standard_normal(n).astype(np.float32))
+                 for n in sizes]
+        delta = [0.5 + i for i in range(len(sizes))]
+        weight = [1.0 / (i + 1) for i in range(len(sizes))]
+        S = m.consistency_score([to_dev(a, dev) for a, _ in comps], [to_dev(b, dev) for _, b in comps],
+                                delta, weight)
+        ref = OM.or_score([OM.or_component_error(a, b, dl) for (a, b), dl in zip(comps, delta)], weight)
+        assert S == pytest.approx(ref, rel=1e-12)
+    finally:
+        m.close()
