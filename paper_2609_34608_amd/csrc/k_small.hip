@@ -771,47 +771,81 @@ __global__ __launch_bounds__(256) void copy_f32x4_kernel(const f32x4* __restrict
 }
 
 // ------------------------------------------------------------- Trajectory Remapping
+// Four consecutive floats p[0 .. cnt) (zeros past cnt): one 16-byte load when
+// VEC (the caller has checked the alignment and cnt == 4), else scalar loads.
+template <bool VEC>
+__device__ __forceinline__ f32x4 load_group(const float* p, int64_t cnt) {
+  if constexpr (VEC) {
+    return *reinterpret_cast<const f32x4*>(p);
+  } else {
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (u < cnt) v[u] = p[u];
+    return v;
+  }
+}
+
+// Float64 sum of ((p - q) * scale)^2 over elements [4 g0, min(4 g1, n)) of a
+// run, by the 256 threads of a block: thread t takes the 4-element groups
+// t, t + 256, ... (four groups in flight per step), and each group's elements
+// in order.  Both instantiations add in exactly this order, so the result
+// does not depend on whether the 16-byte path was taken.
+template <bool VEC>
+__device__ __forceinline__ double run_sq_sum(const float* p, const float* q, double scale, int64_t g0,
+                                             int64_t g1, int64_t n) {
+  const int64_t full = n / 4 < g1 ? n / 4 : g1;  // groups with all four elements
+  double s = 0.0;
+  int64_t g = g0 + threadIdx.x;
+  for (; g + 3 * 256 < full; g += 4 * 256) {
+    f32x4 x[4], y[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      x[u] = load_group<VEC>(p + 4 * (g + u * 256), 4);
+      y[u] = load_group<VEC>(q + 4 * (g + u * 256), 4);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double d = ((double)x[u][e] - (double)y[u][e]) * scale;
+        s = fma(d, d, s);
+      }
+  }
+  for (; g < g1; g += 256) {
+    const int64_t cnt = n - 4 * g < 4 ? n - 4 * g : 4;
+    const f32x4 x = load_group<VEC>(p + 4 * g, VEC ? 4 : cnt), y = load_group<VEC>(q + 4 * g, VEC ? 4 : cnt);
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (e < cnt) {
+        const double d = ((double)x[e] - (double)y[e]) * scale;
+        s = fma(d, d, s);
+      }
+  }
+  return s;
+}
+
 // rms of (x^r - x_bar)/sigma_r per (sample, branch) over the whole branch, in
-// two launches: each branch is cut into reduce_chunks(n) equal runs, one block
-// per run sums its squares (float64); then one block per (sample, branch)
-// adds the run sums in a fixed order (the same bits on every call) and turns
-// the rms into the remap coefficient sigma_b0 / (sigma_r rms) (0 for a zero
-// direction).
+// two launches: each branch is cut into reduce_chunks(n) runs of whole
+// 4-element groups, one block per run sums its squares (float64); then one
+// block per (sample, branch) adds the run sums in a fixed order (the same
+// bits on every call) and turns the rms into the remap coefficient
+// sigma_b0 / (sigma_r rms) (0 for a zero direction).
+template <bool VEC>
 __global__ __launch_bounds__(256) void remap_partial_kernel(RemapArgs a) {
   __shared__ double sh[16];
   const int sb = blockIdx.y;  // sample * 2 + branch
   const int b = sb / 2, br = sb % 2;
   const int64_t traj = (int64_t)a.Nv * a.Cv + (int64_t)a.Na * a.A;
   const int64_t lo = br == 0 ? 0 : (int64_t)a.Nv * a.Cv;
-  const int64_t hi = br == 0 ? (int64_t)a.Nv * a.Cv : traj;
-  const int nch = reduce_chunks(hi - lo);
+  const int64_t n = br == 0 ? (int64_t)a.Nv * a.Cv : (int64_t)a.Na * a.A;
+  const int nch = reduce_chunks(n);
   if ((int)blockIdx.x >= nch) return;
-  const int64_t per = (hi - lo + nch - 1) / nch;
-  const int64_t c0 = lo + (int64_t)blockIdx.x * per;
-  const int64_t c1 = c0 + per < hi ? c0 + per : hi;
-  const float* xr = a.x_r + (size_t)b * traj;
-  const float* xb = a.x_bar + (size_t)b * traj;
-  const double inv = 1.0 / (double)a.sigma_r;
-  double s = 0.0;
-  int64_t i = c0 + threadIdx.x;
-  // eight elements per thread in flight, then the remainder
-  for (; i + 7 * 256 < c1; i += 8 * 256) {
-    float r[8], x[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      r[u] = xr[i + u * 256];
-      x[u] = xb[i + u * 256];
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const double d = ((double)r[u] - (double)x[u]) * inv;
-      s += d * d;
-    }
-  }
-  for (; i < c1; i += 256) {
-    const double d = ((double)xr[i] - (double)xb[i]) * inv;
-    s += d * d;
-  }
+  const int64_t ng = (n + 3) / 4, per = (ng + nch - 1) / nch;
+  const int64_t g0 = (int64_t)blockIdx.x * per;
+  const int64_t g1 = g0 + per < ng ? g0 + per : ng;
+  const size_t off = (size_t)b * traj + lo;
+  double s = run_sq_sum<VEC>(a.x_r + off, a.x_bar + off, 1.0 / (double)a.sigma_r, g0, g1, n);
   s = block_sum_d(s, sh);
   if (threadIdx.x == 0) a.partial[(size_t)sb * kRemapChunks + blockIdx.x] = s;
 }
@@ -838,27 +872,50 @@ __global__ __launch_bounds__(256) void remap_finish_kernel(RemapArgs a) {
 }
 
 // x[j] = x_bar[j+shift] + sigma_b0 d[j+shift] on mapped slots, sigma_b0 eps[j]
-// elsewhere; one element per thread, grid (elements, sample).  Slot j of a
-// branch of width w is mapped when j + shift < slots, i.e. when the element
-// index within the branch plus shift * w stays inside the branch.
+// elsewhere.  Slot j of a branch of width w is mapped when j + shift < slots,
+// i.e. when the element index within the branch plus shift * w stays inside
+// the branch.  Grid (element groups, sample): with VEC each thread takes four
+// consecutive elements with 16-byte loads and stores (the host has checked
+// that the pointers, both branch lengths and both shifted offsets are
+// multiples of four floats, so a group lies in one branch and is mapped or
+// unmapped as a whole); otherwise one element per thread.  Every element is
+// computed by the same expression either way.
+__device__ __forceinline__ float remap_value(float xb, float xr, double coef) {
+  const double x = (double)xb;
+  return (float)(x + ((double)xr - x) * coef);
+}
+
+template <bool VEC>
 __global__ __launch_bounds__(256) void remap_apply_kernel(RemapArgs a) {
   const int64_t traj = (int64_t)a.Nv * a.Cv + (int64_t)a.Na * a.A;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= traj) return;
-  const int b = blockIdx.y;
   const int64_t nv = (int64_t)a.Nv * a.Cv;
-  const bool video = i < nv;
-  const int64_t src = i + (video ? (int64_t)a.shift_video * a.Cv : (int64_t)a.shift_action * a.A);
-  const int64_t end = video ? nv : traj;
+  const int b = blockIdx.y;
   const size_t base = (size_t)b * traj;
-  float out;
-  if (src < end) {
-    const double xb = (double)a.x_bar[base + src];
-    out = (float)(xb + ((double)a.x_r[base + src] - xb) * a.coef[b * 2 + (video ? 0 : 1)]);
+  if constexpr (VEC) {
+    const int64_t i = 4 * ((int64_t)blockIdx.x * 256 + threadIdx.x);
+    if (i >= traj) return;
+    const bool video = i < nv;
+    const int64_t src = i + (video ? (int64_t)a.shift_video * a.Cv : (int64_t)a.shift_action * a.A);
+    f32x4 out;
+    if (src < (video ? nv : traj)) {
+      const f32x4 xb = *reinterpret_cast<const f32x4*>(a.x_bar + base + src);
+      const f32x4 xr = *reinterpret_cast<const f32x4*>(a.x_r + base + src);
+      const double c = a.coef[b * 2 + (video ? 0 : 1)];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) out[e] = remap_value(xb[e], xr[e], c);
+    } else {
+      out = a.sigma_b0 * *reinterpret_cast<const f32x4*>(a.noise + base + i);
+    }
+    *reinterpret_cast<f32x4*>(a.x_out + base + i) = out;
   } else {
-    out = a.sigma_b0 * a.noise[base + i];
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= traj) return;
+    const bool video = i < nv;
+    const int64_t src = i + (video ? (int64_t)a.shift_video * a.Cv : (int64_t)a.shift_action * a.A);
+    a.x_out[base + i] = src < (video ? nv : traj)
+                            ? remap_value(a.x_bar[base + src], a.x_r[base + src], a.coef[b * 2 + (video ? 0 : 1)])
+                            : a.sigma_b0 * a.noise[base + i];
   }
-  a.x_out[base + i] = out;
 }
 
 // ------------------------------------------------------------- Observation Rebinding
@@ -871,38 +928,19 @@ struct OrSumArgs {
 };
 
 // Run sums of ((u_hat - u) / delta)^2 of component blockIdx.y, run blockIdx.x
-// of reduce_chunks(n) (float64); the host adds the runs in order.
+// of reduce_chunks(n) runs of whole 4-element groups (float64, the order of
+// run_sq_sum); the host adds the runs in order.
+template <bool VEC>
 __global__ __launch_bounds__(256) void or_sums_kernel(OrSumArgs a) {
   __shared__ double sh[16];
   const int m = blockIdx.y;
   const int64_t n = a.n[m];
   const int nch = reduce_chunks(n);
   if ((int)blockIdx.x >= nch) return;
-  const int64_t per = (n + nch - 1) / nch;
-  const int64_t c0 = (int64_t)blockIdx.x * per;
-  const int64_t c1 = c0 + per < n ? c0 + per : n;
-  const float* uh = a.u_hat[m];
-  const float* uu = a.u[m];
-  const double idl = a.inv_delta[m];
-  double s = 0.0;
-  int64_t i = c0 + threadIdx.x;
-  for (; i + 7 * 256 < c1; i += 8 * 256) {
-    float p[8], q[8];
-#pragma unroll
-    for (int v = 0; v < 8; ++v) {
-      p[v] = uh[i + v * 256];
-      q[v] = uu[i + v * 256];
-    }
-#pragma unroll
-    for (int v = 0; v < 8; ++v) {
-      const double r = ((double)p[v] - (double)q[v]) * idl;
-      s += r * r;
-    }
-  }
-  for (; i < c1; i += 256) {
-    const double r = ((double)uh[i] - (double)uu[i]) * idl;
-    s += r * r;
-  }
+  const int64_t ng = (n + 3) / 4, per = (ng + nch - 1) / nch;
+  const int64_t g0 = (int64_t)blockIdx.x * per;
+  const int64_t g1 = g0 + per < ng ? g0 + per : ng;
+  double s = run_sq_sum<VEC>(a.u_hat[m], a.u[m], a.inv_delta[m], g0, g1, n);
   s = block_sum_d(s, sh);
   if (threadIdx.x == 0) a.sums[(size_t)m * kRemapChunks + blockIdx.x] = s;
 }
@@ -1075,12 +1113,27 @@ hipError_t launch_copy_f32(const float* src, float* dst, int64_t n, hipStream_t 
   return hipGetLastError();
 }
 
+namespace {
+bool aligned16(const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; }
+}  // namespace
+
 hipError_t launch_remap(const RemapArgs& a, hipStream_t s) {
-  const int nch = std::max(reduce_chunks((int64_t)a.Nv * a.Cv), reduce_chunks((int64_t)a.Na * a.A));
-  launch_k(remap_partial_kernel, dim3(nch, a.B * 2), 256, 0, s, a);
+  const int64_t nv = (int64_t)a.Nv * a.Cv, na = (int64_t)a.Na * a.A, traj = nv + na;
+  // 16-byte path: every group of four floats starts 16-byte aligned in each
+  // array, in its branch and at its shifted source
+  const bool sums_vec = aligned16(a.x_r) && aligned16(a.x_bar) && nv % 4 == 0 && na % 4 == 0;
+  const bool apply_vec = sums_vec && aligned16(a.noise) && aligned16(a.x_out) &&
+                         ((int64_t)a.shift_video * a.Cv) % 4 == 0 && ((int64_t)a.shift_action * a.A) % 4 == 0;
+  const int nch = std::max(reduce_chunks(nv), reduce_chunks(na));
+  if (sums_vec)
+    launch_k(remap_partial_kernel<true>, dim3(nch, a.B * 2), 256, 0, s, a);
+  else
+    launch_k(remap_partial_kernel<false>, dim3(nch, a.B * 2), 256, 0, s, a);
   launch_k(remap_finish_kernel, a.B * 2, 256, 0, s, a);
-  const int64_t traj = (int64_t)a.Nv * a.Cv + (int64_t)a.Na * a.A;
-  launch_k(remap_apply_kernel, dim3((unsigned)((traj + 255) / 256), a.B), 256, 0, s, a);
+  if (apply_vec)
+    launch_k(remap_apply_kernel<true>, dim3((unsigned)((traj / 4 + 255) / 256), a.B), 256, 0, s, a);
+  else
+    launch_k(remap_apply_kernel<false>, dim3((unsigned)((traj + 255) / 256), a.B), 256, 0, s, a);
   return hipGetLastError();
 }
 
@@ -1088,16 +1141,21 @@ hipError_t launch_or_sums(int n_comp, const float* const* u_hat, const float* co
                           const int64_t* n, const double* delta, double* sums, hipStream_t s) {
   if (n_comp < 1 || n_comp > WAM_MAX_COMPONENTS) return hipErrorInvalidValue;
   OrSumArgs a{};
+  bool vec = true;
   for (int m = 0; m < n_comp; ++m) {
     a.u_hat[m] = u_hat[m];
     a.u[m] = u[m];
     a.n[m] = n[m];
     a.inv_delta[m] = 1.0 / delta[m];
+    vec = vec && aligned16(u_hat[m]) && aligned16(u[m]) && n[m] % 4 == 0;
   }
   a.sums = sums;
   int nch = 1;
   for (int m = 0; m < n_comp; ++m) nch = std::max(nch, reduce_chunks(n[m]));
-  launch_k(or_sums_kernel, dim3(nch, n_comp), 256, 0, s, a);
+  if (vec)
+    launch_k(or_sums_kernel<true>, dim3(nch, n_comp), 256, 0, s, a);
+  else
+    launch_k(or_sums_kernel<false>, dim3(nch, n_comp), 256, 0, s, a);
   return hipGetLastError();
 }
 

@@ -109,3 +109,70 @@ def test_consistency_score_max_components(dev):
         assert S == pytest.approx(ref, rel=1e-12)
     finally:
         m.close()
+
+
+def _offset_copy(t, off):
+    """A view of a copy of t that starts `off` floats into a fresh buffer
+    (off = 1: 4-byte aligned only, which sends the kernels down their
+    scalar-load path)."""
+    import torch
+    buf = torch.empty(t.numel() + off, dtype=t.dtype, device=t.device)
+    view = buf[off:].view(t.shape)
+    view.copy_(t)
+    return view
+
+
+@pytest.mark.parametrize("shift_a,shift_v", [(4, 3), (0, 0)])
+def test_remap_vector_and_scalar_paths_agree(dev, shift_a, shift_v):
+    """The remap's 16-byte path (aligned pointers, branch lengths and shifted
+    offsets all multiples of four floats) and its scalar path (the same data
+    one float off alignment) add in the same order and compute each element
+    by the same expression: the outputs agree bit for bit, and with the
+    oracle."""
+    import torch
+    from paper_2609_34608_amd import runtime as R
+    spec = get_workload("tiny").replace(B=2, Nv=100_000, Cv=16, Na=64, A=8)
+    assert (spec.Nv * spec.Cv) % 4 == 0 and (spec.Na * spec.A) % 4 == 0
+    rng = np.random.default_rng(36)
+    xb, xr, eps = (rng.standard_normal((spec.B, spec.traj)).astype(np.float32) for _ in range(3))
+    sr, sb = 0.55, 0.5
+    cfg = R.config_of(spec)
+    outs = []
+    for off in (0, 1):
+        ins = [to_dev(v, dev) for v in (xb, xr, eps)]
+        if off:
+            ins = [_offset_copy(t, off) for t in ins]
+        out = _offset_copy(torch.full((spec.B, spec.traj), float("nan"), device=dev), off)
+        R.remap_noalloc(cfg, ins[0], ins[1], sr, sb, shift_a, shift_v, ins[2], out)
+        outs.append(out.cpu().numpy())
+    np.testing.assert_array_equal(outs[0], outs[1])
+    d = OM.tr_direction(spec, xr, xb, sr)
+    ref = OM.tr_remap(spec, xb, d, sb, shift_a, shift_v, eps)
+    assert rel_err(outs[0], ref) <= 1e-6
+
+
+def test_score_vector_and_scalar_paths_agree(dev):
+    """The rebinding score from aligned components (16-byte loads) and from
+    the same components one float off alignment (scalar loads) is the same
+    float64 value, and the oracle's."""
+    from paper_2609_34608_amd import runtime as R
+    spec = get_workload("tiny")
+    m = R.WamModel(R.config_of(spec), make_weights(spec), device=dev)
+    try:
+        rng = np.random.default_rng(37)
+        comps = [(rng.standard_normal(n).astype(np.float32), rng.standard_normal(n).astype(np.float32))
+                 for n in (1_000_000, 4 * 2 ** 20, 2048)]
+        delta, weight = [2.0, 0.25, 16.0], [0.2, 0.5, 0.3]
+        scores = []
+        for off in (0, 1):
+            uh = [to_dev(a, dev) for a, _ in comps]
+            uu = [to_dev(b, dev) for _, b in comps]
+            if off:
+                uh = [_offset_copy(t, off) for t in uh]
+                uu = [_offset_copy(t, off) for t in uu]
+            scores.append(m.consistency_score(uh, uu, delta, weight))
+        assert scores[0] == scores[1]
+        ref = OM.or_score([OM.or_component_error(a, b, dl) for (a, b), dl in zip(comps, delta)], weight)
+        assert scores[0] == pytest.approx(ref, rel=1e-12)
+    finally:
+        m.close()
