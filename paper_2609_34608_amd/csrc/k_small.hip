@@ -291,55 +291,73 @@ __global__ __launch_bounds__(256) void ln_modulate_v4_kernel(const float* __rest
 }
 
 // ------------------------------------------------------------- final layer + Euler
-// One wave per group of R trajectory rows of one branch of one sample, so the
-// rows share the branch's head weights (W^T packed [Cout][D]).  A lane holds
-// elements VEC lane + 64 VEC i .. + VEC-1 of each row.  Every load that does
-// not depend on a reduction is issued up front (the rows, the modulation) and
-// the head weights arrive one column chunk at a time for all 16 channels, so a
-// wave waits on memory only 1 + D / (64 VEC) times.  Each lane forms partial
-// products of its elements for R rows x 16 channels; butterfly sums over the
-// 64 lanes leave lane l < 16 R with the full dot product of row l / 16,
-// channel l % 16, which it stores as the velocity and/or applies as the Euler
-// update x += dsigma v.
+// A block of NW waves takes NW R consecutive trajectory rows of one branch of
+// one sample, wave w the rows w R .. w R + R-1, so that all of them share the
+// branch's head weights (W^T packed [Cout][D]) and the modulation vectors,
+// which the block copies from global memory into LDS once.  A lane holds elements VEC lane + 64 VEC i ..
+// + VEC-1 of each row.  Every load that does not depend on a reduction is
+// issued up front (the rows, the modulation, the weight copy).  Each lane
+// forms partial products of its elements for R rows x 16 channels; butterfly
+// sums over the 64 lanes leave lane l < 16 R with the full dot product of row
+// l / 16, channel l % 16, which it stores as the velocity and/or applies as
+// the Euler update x += dsigma v.
 constexpr int kFinalCout = 16;
-template <int VEC, int R, int MAXC>
-__global__ __launch_bounds__(256) void final_kernel(FinalArgs a) {
-  using vec = float __attribute__((ext_vector_type(VEC)));
-  const int lane = threadIdx.x % kWave;
-  const int wave = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
-  const int gv = (a.Nv + R - 1) / R, ga = (a.Na + R - 1) / R;
-  int b, t0, tend;
-  bool video;
-  if (wave < a.B * gv) {
-    b = wave / gv;
-    t0 = (wave % gv) * R;
-    tend = a.Nv;
-    video = true;
-  } else {
-    const int w = wave - a.B * gv;
-    if (w >= a.B * ga) return;
-    b = w / ga;
-    t0 = a.Nv + (w % ga) * R;
-    tend = a.Nv + a.Na;
-    video = false;
+template <int VEC>
+using fvec = float __attribute__((ext_vector_type(VEC)));
+
+// Copies n floats (a multiple of 4) from global memory to LDS with
+// direct-to-LDS 16-byte loads, 1 KiB per instruction, runs c = first, first +
+// step, ...: lanes past the end of the last run re-read the final 16 bytes,
+// into LDS that is never read (the destination is sized in whole runs).
+__device__ __forceinline__ void copy_to_lds(const float* src, float* dst, int n, int lane, int first, int step) {
+  for (int c = first; c * 256 < n; c += step) {
+    const int e = c * 256 + 4 * lane;
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(src + (e < n ? e : n - 4)),
+                                     (__attribute__((address_space(3))) void*)(dst + c * 256), 16, 0, 0);
   }
+}
+
+// D a multiple of 64 VEC, at most 64 VEC MAXC.  Each wave first requests its
+// rows (HBM; rows at or past the branch end re-read the group's first row and
+// are never stored), then the block copies the Cout x D weights (contiguous,
+// the same layout in LDS) and the modulation vectors into LDS; after a full
+// wait and the barrier each wave reads its columns of them from LDS.
+template <int VEC, int R, int MAXC, int NW>
+__global__ __launch_bounds__(NW * 64) void final_kernel(FinalArgs a) {
+  using vec = fvec<VEC>;
+  constexpr int DMAX = MAXC * 64 * VEC;  // a multiple of 256
+  __shared__ __attribute__((aligned(1024))) float wsm[kFinalCout * DMAX];
+  __shared__ __attribute__((aligned(1024))) float msc[DMAX], msh[DMAX];
+  const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
+  constexpr int RB = NW * R;  // rows per block
+  const int gv = (a.Nv + RB - 1) / RB, ga = (a.Na + RB - 1) / RB, per = gv + ga;
+  const int b = blockIdx.x / per, j = blockIdx.x % per;
+  const bool video = j < gv;
+  const int t0 = (video ? j * RB : a.Nv + (j - gv) * RB) + wid * R;
+  const int tend = video ? a.Nv : a.Nv + a.Na;
+  const bool active = t0 < tend;  // waves past the branch end only help with the copies
   const int nch = a.D / (kWave * VEC);
   auto col = [&](int i) { return VEC * lane + kWave * VEC * i; };
-  vec u[R][MAXC], sc[MAXC], sh[MAXC];
+  vec u[R][MAXC];
+  if (active) {
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    // rows past the branch end re-read the group's first row (never stored)
-    const float* hr = a.h + ((size_t)b * a.T + (t0 + r < tend ? t0 + r : t0)) * a.D;
+    for (int r = 0; r < R; ++r) {
+      const float* hr = a.h + ((size_t)b * a.T + (t0 + r < tend ? t0 + r : t0)) * a.D;
 #pragma unroll
-    for (int i = 0; i < MAXC; ++i)
-      if (i < nch) u[r][i] = *reinterpret_cast<const vec*>(hr + col(i));
-  }
-#pragma unroll
-  for (int i = 0; i < MAXC; ++i)
-    if (i < nch) {
-      sc[i] = *reinterpret_cast<const vec*>(a.scale + col(i));
-      sh[i] = *reinterpret_cast<const vec*>(a.shift + col(i));
+      for (int i = 0; i < MAXC; ++i)
+        if (i < nch) u[r][i] = *reinterpret_cast<const vec*>(hr + col(i));
     }
+  }
+  const int cout = video ? a.Cv : a.A;
+  copy_to_lds(video ? a.wv : a.wa, wsm, cout * a.D, lane, wid, NW);
+  copy_to_lds(a.scale, msc, a.D, lane, (wid + NW - 1) % NW, NW);
+  copy_to_lds(a.shift, msh, a.D, lane, (wid + NW - 2) % NW, NW);
+  // the compiler does not track the LDS writes of those loads: wait for all
+  // of this wave's memory operations, then for every wave's
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (!active) return;
+
   float mean[R], rstd[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
@@ -348,7 +366,7 @@ __global__ __launch_bounds__(256) void final_kernel(FinalArgs a) {
     for (int i = 0; i < MAXC; ++i)
       if (i < nch)
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) s += u[r][i][j];
+        for (int e = 0; e < VEC; ++e) s += u[r][i][e];
     mean[r] = wave_sum(s) / (float)a.D;
   }
 #pragma unroll
@@ -358,56 +376,57 @@ __global__ __launch_bounds__(256) void final_kernel(FinalArgs a) {
     for (int i = 0; i < MAXC; ++i)
       if (i < nch)
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) {
-          const float dv = u[r][i][j] - mean[r];
+        for (int e = 0; e < VEC; ++e) {
+          const float dv = u[r][i][e] - mean[r];
           q += dv * dv;
         }
     rstd[r] = rsqrtf(wave_sum(q) / (float)a.D + a.eps);
   }
 #pragma unroll
-  for (int r = 0; r < R; ++r)
+  for (int i = 0; i < MAXC; ++i)
+    if (i < nch) {
+      const vec sc = *reinterpret_cast<const vec*>(msc + col(i));
+      const vec sh = *reinterpret_cast<const vec*>(msh + col(i));
 #pragma unroll
-    for (int i = 0; i < MAXC; ++i)
-      if (i < nch) u[r][i] = (u[r][i] - mean[r]) * rstd[r] * (1.0f + sc[i]) + sh[i];
-  const int cout = video ? a.Cv : a.A;
-  const float* W = video ? a.wv : a.wa;
+      for (int r = 0; r < R; ++r) u[r][i] = (u[r][i] - mean[r]) * rstd[r] * (1.0f + sc) + sh;
+    }
   constexpr int NV = R * kFinalCout;  // partial sums per lane, index r * 16 + o
   float v[NV];
 #pragma unroll
-  for (int j = 0; j < NV; ++j) v[j] = 0.f;
+  for (int k = 0; k < NV; ++k) v[k] = 0.f;
 #pragma unroll
   for (int i = 0; i < MAXC; ++i) {
     if (i < nch) {
       vec w[kFinalCout];
 #pragma unroll
       for (int o = 0; o < kFinalCout; ++o)
-        w[o] = o < cout ? *reinterpret_cast<const vec*>(W + (size_t)o * a.D + col(i)) : vec(0.f);
+        w[o] = o < cout ? *reinterpret_cast<const vec*>(wsm + o * a.D + col(i)) : vec(0.f);
 #pragma unroll
       for (int r = 0; r < R; ++r)
 #pragma unroll
         for (int o = 0; o < kFinalCout; ++o) {
           const vec p = u[r][i] * w[o];
 #pragma unroll
-          for (int j = 0; j < VEC; ++j) v[r * kFinalCout + o] += p[j];
+          for (int e = 0; e < VEC; ++e) v[r * kFinalCout + o] += p[e];
         }
     }
   }
   // lane bits above NV: plain butterfly sums; then a reduce-scatter, where
-  // after the step over lane bit s, v[j] (j < s) holds the partial sum of
-  // index j + (lane & s) + the bits already consumed.  Lane l ends with the
+  // after the step over lane bit s, v[k] (k < s) holds the partial sum of
+  // index k + (lane & s) + the bits already consumed.  Lane l ends with the
   // full sum of index l % NV.
 #pragma unroll
   for (int s = kWave / 2; s >= NV; s >>= 1)
 #pragma unroll
-    for (int j = 0; j < NV; ++j) v[j] += __shfl_xor(v[j], s, 64);
+    for (int k = 0; k < NV; ++k) v[k] += __shfl_xor(v[k], s, 64);
 #pragma unroll
   for (int s = NV / 2; s >= 1; s >>= 1) {
     const bool hi = (lane & s) != 0;
 #pragma unroll
-    for (int j = 0; j < s; ++j) {
-      const float keep = hi ? v[j + s] : v[j];
-      const float send = hi ? v[j] : v[j + s];
-      v[j] = keep + __shfl_xor(send, s, 64);
+    for (int k = 0; k < s; ++k) {
+      const float keep = hi ? v[k + s] : v[k];
+      const float send = hi ? v[k] : v[k + s];
+      v[k] = keep + __shfl_xor(send, s, 64);
     }
   }
   const int r = lane / kFinalCout, o = lane % kFinalCout, t = t0 + r;
@@ -420,59 +439,6 @@ __global__ __launch_bounds__(256) void final_kernel(FinalArgs a) {
   if (a.x) a.x[idx] += a.dsigma * vel;
 }
 
-// General form (any D % 64 == 0): four trajectory rows per wave; lane =
-// (row r = lane/16, output channel o = lane%16).  The 16 lanes of a row compute its LayerNorm statistics
-// together, stage the modulated row in LDS, then each lane forms one output
-// v[r][o] = u[r] . W^T[o] + b[o] (W^T packed [Cout][D], read through L1/L2),
-// stores the velocity and/or applies the Euler update x += dsigma v.
-constexpr int kFinalWaves = 1;
-__global__ __launch_bounds__(kFinalWaves * 64) void final_rows_kernel(FinalArgs a) {
-  extern __shared__ float us[];  // [kFinalWaves * 4][D]
-  const int nrow = a.Nv + a.Na;
-  const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
-  const int r = lane / 16, o = lane % 16;
-  const int grow = (blockIdx.x * kFinalWaves + wid) * 4 + r;  // global trajectory row
-  const bool valid = grow < a.B * nrow;
-  const int b = valid ? grow / nrow : 0, t = valid ? grow % nrow : 0;
-  float* ur = us + (size_t)(wid * 4 + r) * a.D;
-  const float* hr = a.h + ((size_t)b * a.T + t) * a.D;
-  // LayerNorm statistics over the 16 lanes of this row (xor < 16 stays in the row)
-  float s = 0.f;
-  for (int c = o; c < a.D; c += 16) s += valid ? hr[c] : 0.f;
-#pragma unroll
-  for (int m = 8; m > 0; m >>= 1) s += __shfl_xor(s, m, 64);
-  const float mean = s / (float)a.D;
-  float q = 0.f;
-  for (int c = o; c < a.D; c += 16) {
-    const float d = (valid ? hr[c] : 0.f) - mean;
-    q += d * d;
-  }
-#pragma unroll
-  for (int m = 8; m > 0; m >>= 1) q += __shfl_xor(q, m, 64);
-  const float rstd = rsqrtf(q / (float)a.D + a.eps);
-  for (int c = o; c < a.D; c += 16)
-    ur[c] = valid ? (hr[c] - mean) * rstd * (1.0f + a.scale[c]) + a.shift[c] : 0.f;
-  __syncthreads();
-  const bool video = t < a.Nv;
-  const int cout = video ? a.Cv : a.A;
-  if (!valid || o >= cout) return;
-  const float* w = (video ? a.wv : a.wa) + (size_t)o * a.D;
-  // D % 64 == 0: 16 independent 16-byte weight loads in flight per step
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int c0 = 0; c0 < a.D; c0 += 64) {
-    f32x4 wv[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) wv[i] = *reinterpret_cast<const f32x4*>(w + c0 + 4 * i);
-#pragma unroll
-    for (int i = 0; i < 16; ++i) acc += *reinterpret_cast<const f32x4*>(ur + c0 + 4 * i) * wv[i];
-  }
-  const float vel = (acc[0] + acc[1]) + (acc[2] + acc[3]) + (video ? a.bv : a.ba)[o];
-  const int traj = a.Nv * a.Cv + a.Na * a.A;
-  const size_t idx = (size_t)b * traj + (video ? (size_t)t * a.Cv + o
-                                               : (size_t)a.Nv * a.Cv + (size_t)(t - a.Nv) * a.A + o);
-  if (a.v_out) a.v_out[idx] = vel;
-  if (a.x) a.x[idx] += a.dsigma * vel;
-}
 
 // ------------------------------------------------------------- Residual Rescaling
 // Per row: sums of p_i p_a, p_i^2, p_a^2 with p_i = h_s - h_q (float64), one
@@ -1016,34 +982,40 @@ hipError_t launch_ln_modulate(const float* h, const float* shift, const float* s
   return hipGetLastError();
 }
 
-template <int VEC, int R, int MAXC>
+template <int VEC, int R, int MAXC, int NW = 8>
 void launch_final_t(const FinalArgs& a, hipStream_t s) {
-  const int waves = a.B * ((a.Nv + R - 1) / R + (a.Na + R - 1) / R);
-  if (waves > 0) launch_k(final_kernel<VEC, R, MAXC>, (waves + 3) / 4, 256, 0, s, a);
+  constexpr int RB = NW * R;
+  const int blocks = a.B * ((a.Nv + RB - 1) / RB + (a.Na + RB - 1) / RB);
+  if (blocks > 0) launch_k(final_kernel<VEC, R, MAXC, NW>, blocks, NW * 64, 0, s, a);
 }
 
 hipError_t launch_final(const FinalArgs& a, hipStream_t s) {
-  if (a.D % kWave || a.D / kWave > kMaxVpl || a.Cv > kFinalCout || a.A > kFinalCout) return hipErrorInvalidValue;
-  // widest column vector D allows; rows per wave within the register budget
-  if (a.D % (4 * kWave) == 0) {
-    // four rows per wave share each head-weight chunk; short trajectories
-    // (under 4096 rows: 200 waves of four rows on the small model) take one
-    // row per wave instead, so that enough waves hide the memory latency
-    if (a.D <= 1536 && (long)a.B * (a.Nv + a.Na) >= 4096)
-      launch_final_t<4, 4, 6>(a, s);
+  if (a.D % kWave || a.D > 2048 || a.Cv > kFinalCout || a.A > kFinalCout) return hipErrorInvalidValue;
+  // the widest column vector D allows; the smallest LDS copy that holds the
+  // weights (48 KB at D <= 768, so that several blocks share a CU); four rows
+  // per wave share each weight read (two where the rows' registers would not
+  // fit), or one row per wave for short trajectories (under 4096 rows: the
+  // small model's 800 rows as 100 blocks of 8)
+  const bool many = (long)a.B * (a.Nv + a.Na) >= 4096;
+  if (a.D % 256 == 0) {
+    if (a.D <= 768)
+      many ? launch_final_t<4, 4, 3>(a, s) : launch_final_t<4, 1, 3>(a, s);
+    else if (a.D <= 1024)
+      many ? launch_final_t<4, 4, 4>(a, s) : launch_final_t<4, 1, 4>(a, s);
     else if (a.D <= 1536)
-      launch_final_t<4, 1, 6>(a, s);
+      many ? launch_final_t<4, 4, 6>(a, s) : launch_final_t<4, 1, 6>(a, s);
     else
       launch_final_t<4, 2, 8>(a, s);
-  } else if (a.D % (2 * kWave) == 0 && a.D <= 1024) {
-    launch_final_t<2, 4, 8>(a, s);
-  } else if (a.D <= 1024) {
-    launch_final_t<1, 2, 16>(a, s);
+  } else if (a.D % 128 == 0) {
+    if (a.D <= 1024)
+      many ? launch_final_t<2, 4, 8>(a, s) : launch_final_t<2, 1, 8>(a, s);
+    else
+      launch_final_t<2, 2, 16>(a, s);
   } else {
-    const int rows = a.B * (a.Nv + a.Na);
-    const int per_block = kFinalWaves * 4;
-    const size_t lds = (size_t)per_block * a.D * sizeof(float);
-    launch_k(final_rows_kernel, (rows + per_block - 1) / per_block, kFinalWaves * 64, lds, s, a);
+    if (a.D <= 1024)
+      many ? launch_final_t<1, 4, 16>(a, s) : launch_final_t<1, 1, 16>(a, s);
+    else
+      launch_final_t<1, 2, 32>(a, s);
   }
   return hipGetLastError();
 }

@@ -57,13 +57,27 @@ def test_tiny_velocity_each_step(dev):
         assert rel_err(v.cpu().numpy(), ref) <= FP32_TOL, k
 
 
-@pytest.mark.parametrize("D,H", [(192, 3), (1088, 17), (2048, 32)])
-def test_hidden_sizes_velocity(dev, D, H):
-    """Velocity within 1e-4 at hidden sizes that select each form of the
-    final-layer kernel (8-byte columns up to 1024 wide, the general
-    per-row form, two rows per wave at 2048), on the tiny token layout."""
+# (D, H, B, Nv): every instantiation of the final-layer kernel (column vector
+# of 16, 8 or 4 bytes for D a multiple of 256, 128 or 64; 1, 2 or 4 rows per
+# wave; the LDS copy of the head weights sized for D up to 768, 1024, 1536 or
+# 2048), on the tiny token layout with L = 1.  B (Nv + Na) >= 4096 rows
+# selects four rows per wave.
+_FINAL_FORMS = [
+    (192, 3, 1, 64), (1088, 17, 1, 64), (2048, 32, 1, 64),   # 4 B x 1 row, 4 B x 2, 16 B x 2
+    (768, 12, 1, 64), (256, 4, 4, 1024),                     # 16 B, D <= 768: 1 and 4 rows
+    (1024, 16, 1, 64), (1024, 16, 4, 1024),                  # 16 B, D <= 1024
+    (1536, 24, 1, 64), (1536, 24, 4, 1024),                  # 16 B, D <= 1536
+    (384, 6, 1, 64), (384, 6, 4, 1024), (1152, 18, 1, 64),   # 8 B: 1, 4 and 2 rows
+    (320, 5, 4, 1024),                                       # 4 B x 4 rows
+]
+
+
+@pytest.mark.parametrize("D,H,B,Nv", _FINAL_FORMS)
+def test_hidden_sizes_velocity(dev, D, H, B, Nv):
+    """Velocity within 1e-4 at hidden sizes and row counts that select each
+    form of the final-layer kernel."""
     from paper_2609_34608_amd import runtime as R
-    spec = get_workload("tiny").replace(D=D, H=H, L=1)
+    spec = get_workload("tiny").replace(D=D, H=H, L=1, B=B, Nv=Nv)
     W = make_weights(spec, bias_std=0.02)
     m = R.WamModel(R.config_of(spec), W, device=dev)
     sig = f32_sigmas(spec.K)
