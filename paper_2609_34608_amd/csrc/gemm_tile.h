@@ -84,6 +84,7 @@ __device__ __forceinline__ void epi4(const GemmArgs& a, int m, int n, float v0, 
     float4 hv = *h;
     hv.x += g.x * v0; hv.y += g.y * v1; hv.z += g.z * v2; hv.w += g.w * v3;
     *h = hv;
+    if (a.copy) *reinterpret_cast<float4*>(a.copy + (size_t)m * a.N + n) = hv;
   } else if constexpr (EPI == EPI_BIAS_GELU) {
     store_bf16x4(static_cast<bf16*>(a.out) + (size_t)m * a.N + n, gelu_tanh_f(v0), gelu_tanh_f(v1),
                  gelu_tanh_f(v2), gelu_tanh_f(v3));
@@ -185,13 +186,22 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, const f32x4 (&acc)
       const int m = mb + i * 16 + lr;
       if (m >= a.M) continue;
       if constexpr (EPI == EPI_GATED_RES) {
-        // residual stream h += gate * (acc + bias): all loads of the row first
-        f32x4* hrow = reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + (size_t)m * a.N + nb + lg * 4);
+        // residual stream h += gate * (acc + bias): all loads of the row first;
+        // with a copy target the new values are stored there as well
+        const size_t off = (size_t)m * a.N + nb + lg * 4;
+        f32x4* hrow = reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + off);
         f32x4 hv[TN];
 #pragma unroll
         for (int j = 0; j < TN; ++j) hv[j] = hrow[j * 4];
 #pragma unroll
-        for (int j = 0; j < TN; ++j) hrow[j * 4] = hv[j] + gate[j] * (acc[j][i] + bias[j]);
+        for (int j = 0; j < TN; ++j) hv[j] = hv[j] + gate[j] * (acc[j][i] + bias[j]);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) hrow[j * 4] = hv[j];
+        if (a.copy) {
+          f32x4* crow = reinterpret_cast<f32x4*>(a.copy + off);
+#pragma unroll
+          for (int j = 0; j < TN; ++j) crow[j * 4] = hv[j];
+        }
       } else {
         bf16* orow = static_cast<bf16*>(a.out) + (size_t)m * a.N + nb + lg * 4;
 #pragma unroll

@@ -95,7 +95,9 @@ __device__ __forceinline__ void epi1_f32(const GemmArgs& a, int m, int n, float 
   const float v = acc + a.bias[n];
   if constexpr (EPI == EPI_GATED_RES) {
     float* h = static_cast<float*>(a.out) + (size_t)m * a.N + n;
-    *h += a.gate[n] * v;
+    const float nv = *h + a.gate[n] * v;
+    *h = nv;
+    if (a.copy) a.copy[(size_t)m * a.N + n] = nv;
   } else if constexpr (EPI == EPI_BIAS_GELU) {
     static_cast<float*>(a.out)[(size_t)m * a.N + n] = gelu_tanh_f(v);
   } else {

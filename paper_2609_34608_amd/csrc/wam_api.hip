@@ -360,7 +360,9 @@ int embed(wam_t h, const float* x, const float* cond) {
   return WAM_OK;
 }
 
-int run_layer(wam_t h, int l, const int* skip = nullptr) {
+// copy: when non-null, the layer's MLP-down epilogue (the last writer of h)
+// also stores the layer's output h there.
+int run_layer(wam_t h, int l, const int* skip = nullptr, float* copy = nullptr) {
   const Dims& d = h->d;
   const DevLayout& wl = h->wl;
   const WsLayout& ws = h->ws;
@@ -431,7 +433,7 @@ int run_layer(wam_t h, int l, const int* skip = nullptr) {
   {
     ProfScope ps(h, WAM_KC_GEMM_FC2, 2.0 * M * D * d.F);
     GemmArgs g{h->S<char>(ws.mlp), fc2_w, fc2_b, mod + 5 * D, hh, d.M, (int)D, d.F, EPI_GATED_RES, 3,
-               h->S(ws.gsplit), {}, skip};
+               h->S(ws.gsplit), {}, skip, copy};
     HIPCHK(h, launch_gemm(g, d.bf, s));
   }
   return WAM_OK;
@@ -501,8 +503,9 @@ int enqueue_step_device(wam_t h, int k, const float* x, const float* cond, float
     if ((st = run_layers(h, 0, d.L))) return st;
     return final_step(h, k, v_out, x_euler);
   }
-  if ((st = run_layers(h, 0, rr->q))) return st;
-  HIPCHK(h, launch_copy_f32(hh, h->S(ws.hq), MD, s));
+  // the head [0, q): the last layer's MLP-down epilogue also writes h_q
+  if ((st = run_layers(h, 0, rr->q - 1))) return st;
+  if ((st = run_layer(h, rr->q - 1, nullptr, h->S(ws.hq)))) return st;
   if ((st = run_layers(h, rr->q, rr->s))) return st;
   const int* flag = nullptr;
   if (attempt) {
@@ -618,8 +621,9 @@ int forward(wam_t h, int k, const float* x, const float* cond, float* v_out, flo
     if ((st = run_layers(h, 0, d.L))) return st;
   } else {
     in->rr_active = 1;
-    if ((st = run_layers(h, 0, rr->q))) return st;
-    HIPCHK(h, launch_copy_f32(hh, h->S(ws.hq), MD, s));
+    // the head [0, q): the last layer's MLP-down epilogue also writes h_q
+    if ((st = run_layers(h, 0, rr->q - 1))) return st;
+    if ((st = run_layer(h, rr->q - 1, nullptr, h->S(ws.hq)))) return st;
     if ((st = run_layers(h, rr->q, rr->s))) return st;
     bool accept = false;
     const RRRows br = rr_rows(d, rr);

@@ -135,6 +135,7 @@ struct GemmArgs {
   float* partial;    // split-K scratch, splits * M * N floats
   QkvOut qkv;
   const int* skip;   // device flag: when non-null and set, the launch does nothing
+  float* copy;       // EPI_GATED_RES: when non-null, the updated h is also stored here ([M][N])
 };
 
 struct GemmPlan {
