@@ -1,5 +1,6 @@
 """Residual Rescaling at the mid (B = 4, T = 2306) and large (T = 10176)
-shapes against the oracle, teacher-forced on the device's own hidden states.
+shapes, and on a short sequence whose projections split K over blocks,
+against the oracle, teacher-forced on the device's own hidden states.
 
 Step 0 runs with the layer state empty: every layer is computed and the
 state is established, p_a = h_s - h_q and R_a = h_e - h_s (Eq. crr-reference).
@@ -25,7 +26,7 @@ import numpy as np
 import pytest
 
 from oracle import dit as OD, method as OM
-from synth import make_initial_noise, make_observations
+from synth import get_workload, make_initial_noise, make_observations, make_weights
 from gpu_common import device, to_dev, rel_err, f32_sigmas, model_for, rr_of
 
 pytestmark = pytest.mark.gpu
@@ -43,11 +44,24 @@ def _say(name, t0, what):
     print(f"[{name} {time.time() - t0:6.1f} s] {what}", flush=True)
 
 
-@pytest.mark.parametrize("name", ["mid", "large"])
+def _model(name, dev):
+    """The workload's cached model, or for "small_short" the small model on
+    a 64-token sequence with two samples: its 128 rows make the attention
+    output and MLP-down projections split K over blocks, so the head's h_q
+    is stored by the split reduce pass rather than the tile epilogue."""
+    if name != "small_short":
+        return model_for(name, dev)
+    from paper_2609_34608_amd import runtime as R
+    spec = get_workload("small").replace(B=2, Nv=24, No=8)
+    W = make_weights(spec)
+    return spec, W, R.WamModel(R.config_of(spec), W, device=dev)
+
+
+@pytest.mark.parametrize("name", ["small_short", "mid", "large"])
 def test_full_size_rr_gate_and_injection(dev, name):
     from paper_2609_34608_amd import _lib as L
     t0 = time.time()
-    spec, W, m = model_for(name, dev)
+    spec, W, m = _model(name, dev)
     q, s, e = spec.rr_bounds
     sig = f32_sigmas(spec.K)
     m.set_schedule(sig)
@@ -111,6 +125,8 @@ def test_full_size_rr_gate_and_injection(dev, name):
             assert moved >= 10 * BF16_TOL, moved
     finally:
         OD.ATTENTION_THREADS = threads
+        if name == "small_short":
+            m.close()
 
 
 @pytest.mark.parametrize("name", ["small", "mid", "large"])
