@@ -97,3 +97,49 @@ def test_committed_traffic_summaries_are_complete():
         assert set(t["classes"]) == set(bench.CLASS_NAMES), w
         assert len(t["commands"]) == 2 and "FETCH_SIZE" in t["commands"][0] and "WRITE_SIZE" in t["commands"][1]
         assert t["classes"]["attention"]["traffic_bytes"] > 0
+
+
+@pytest.mark.parametrize("name", ["small", "mid", "large"])
+def test_class_flops_follow_the_layer_formula(name):
+    """The four projections of a layer add up to 24 B T D^2 (F = 4 D) and
+    attention is 4 B T^2 D; at the large model 576.2 and 636.2 GFLOP."""
+    from synth import get_workload
+    spec = get_workload(name)
+    gemm = sum(bench.class_flops(spec, c) for c in ("gemm_qkv", "gemm_proj", "gemm_fc1", "gemm_fc2"))
+    assert spec.F == 4 * spec.D
+    assert gemm == 24.0 * spec.B * spec.T * spec.D ** 2
+    assert bench.class_flops(spec, "attention") == 4.0 * spec.B * spec.T ** 2 * spec.D
+    if name == "large":
+        assert round(gemm / 1e9, 1) == 576.2
+        assert round(bench.class_flops(spec, "attention") / 1e9, 1) == 636.2
+
+
+def test_mfma_summary_formulas(tmp_path, monkeypatch):
+    """Hardware FLOP = MOPS x 512; MFMA busy = busy cycles over one XCD's
+    active cycles (GRBM_GUI_ACTIVE / 8) x 1024 SIMDs; clock = those cycles
+    over the dispatch time."""
+    from synth import get_workload
+    (tmp_path / "profiles").mkdir()
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    spec = get_workload("large")
+    name = "void wam::gemm::gemm_bf16_kernel<256, 256, 2, 4, 2, 64, 3, 0, false>(wam::GemmArgs)"
+    ns = 130_000.0  # one dispatch of 130 us
+    active = 2.4 * ns  # cycles of one XCD at 2.4 GHz
+    mops = bench.class_flops(spec, "gemm_qkv") / 512.0
+    busy = 0.5 * active * 1024
+    csv_path = tmp_path / "mfma.csv"
+    with open(csv_path, "w") as f:
+        f.write(",".join(_FIELDS) + "\n")
+        for counter, value in (("SQ_INSTS_VALU_MFMA_MOPS_BF16", mops), ("SQ_VALU_MFMA_BUSY_CYCLES", busy),
+                               ("GRBM_GUI_ACTIVE", 8 * active), ("SQ_BUSY_CU_CYCLES", 1.0)):
+            f.write(f'7,"{name}",{counter},{value},0,{int(ns)}\n')
+    bench.summarize_mfma(str(csv_path), "large", ["pmc cmd"])
+    text = (tmp_path / "profiles" / "mfma_counters_large.md").read_text()
+    row = [r for r in text.splitlines() if r.startswith("| gemm_qkv")][0].split("|")
+    cells = [c.strip() for c in row[1:-1]]
+    # class, dispatches, avg us, alg GFLOP, hw GFLOP, hw/alg, TFLOP/s, % of peak, busy, clock, issue
+    assert cells[1] == "1" and cells[2] == "130.00"
+    assert cells[3] == cells[4] == "144.05" and cells[5] == "1.0000"
+    assert cells[8] == "50.0%" and cells[9] == "2.400"
+    assert cells[6] == f"{bench.class_flops(spec, 'gemm_qkv') / ns / 1e3:.1f}"
+    assert "pmc cmd" in text
